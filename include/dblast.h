@@ -1,0 +1,197 @@
+/*
+ * dblast.h - C ABI of the DBLast head + stochastic verification library for AMD gfx950.
+ *
+ * DBLast ("Dependent Block Drafting for Stochastic Speculative Decoding") drafts a block of K
+ * tokens from a low-rank latent mixture over R categories,
+ *
+ *     q(x_1..x_K | y) = sum_z q(z | y) prod_k q_k(x_k | y, z)                 (Eq. cp-drafter)
+ *
+ * where every branch distribution q_k(. | y, z) is the softmax of the shared target LM head
+ * applied to a category-specific hidden state (Sec. "Architecture"), and verifies it against
+ * the target with the prefix-marginalised conditional (Eqs. dep-conditional,
+ * category-posterior, dep-next-token-distribution) in the sequential accept/residual loop of
+ * speculative sampling (Eq. accept-prob; Sec. "Distributional correctness"). This library runs
+ * that path on the GPU:
+ *
+ *   dbl_head_logprobs   branch log-probabilities over the vocabulary (head GEMM + log-softmax)
+ *   dbl_sample_block    category and token draw of one block per sequence
+ *   dbl_verify_block    sequential accept test, residual or bonus draw, acceptance mass
+ *   dbl_expected_len    acceptance mass and expected accepted length along a given trajectory
+ *
+ * Notation. B blocks (one per sequence), K drafted positions, R categories, d hidden size, V
+ * vocabulary size. The paper writes b for the block length and K for the number of categories.
+ * Row m of the branch hidden states and of every per-row output is m = (b*K + k)*R + r, and
+ * M = B*K*R. Vocabulary tiles are DBL_VTILE = 128 consecutive ids: tile t holds ids
+ * [128 t, min(128 t + 128, V)); nT = ceil(V / 128).
+ *
+ * Branch log-probabilities are handed over in a two-level form that one pass over V can
+ * write without storing logits: for row m and id v in tile t,
+ *     lmass[m*nT + t] = log sum_{u in t} exp(logit[m, u])   (tile log-mass)
+ *     tls[m*V + v]    = logit[m, v] - lmass[m*nT + t]        (log-prob of v within its tile)
+ *     lse[m]          = log sum_u exp(logit[m, u])
+ * and every consumer uses the binary32 value  lq(m, v) = fl32(tls + fl32(lmass - lse)).
+ *
+ * Random draws and discrete decisions follow one determinism contract, so that an
+ * independent implementation reproduces every token index bit for bit:
+ *  - draws: word 0 of Philox4x32-10 (Salmon et al., SC'11) with counter
+ *    (k, purpose, seq mod 2^32, step mod 2^32) and key (seed low 32 bits, seed high 32 bits);
+ *    purposes: 0 category, 1 drafted token, 2 accept coin, 3 residual or bonus token;
+ *    seq = seq_offset + b (a per-sequence stream);
+ *  - probabilities that decide are computed with a deterministic exponential built from
+ *    separately rounded IEEE operations (binary32 for token probabilities, binary64 for the
+ *    category weights), quantised as floor(p * 2^40) and compared or summed as integers;
+ *  - the category posterior is normalised in the log domain with an ascending-z sum; the
+ *    mixture at a token is the binary64 sum over ascending z of w_z * q_z;
+ *  - an inverse-CDF draw on integer weights W with word r picks the smallest index whose
+ *    inclusive cumulative weight exceeds floor(r * sum(W) / 2^32); a position is accepted iff
+ *    r * Q < P * 2^32 for the quantised proposal Q and target P at the drafted token.
+ *
+ * Conventions for every call:
+ *  - Ownership: every data pointer is a device pointer owned by the caller; the library never
+ *    allocates device memory. Scratch space is a caller-provided device workspace of at least
+ *    dbl_workspace_bytes(op, shape) bytes, 256-byte aligned.
+ *  - Streams: work is enqueued on `stream` (a hipStream_t; NULL is the default stream) and the
+ *    call returns without waiting. Outputs are valid once the stream reaches that point.
+ *  - Errors: a non-zero dbl_status is returned before anything is launched when an argument is
+ *    invalid; DBL_EHIP reports a failed launch. dbl_last_error() gives a message for the
+ *    calling thread's last failure. Data-dependent problems (NaN inputs) are not detected.
+ *  - Shapes: K, R, d, V >= 1, B >= 0 (B = 0 is a no-op), R <= 64, V < 2^24, d % 8 == 0 for the
+ *    head, M * V < 2^62.
+ *  - Thread safety: calls hold no global mutable state apart from the per-thread error text;
+ *    concurrent calls on different streams with disjoint outputs and workspaces are safe.
+ */
+#ifndef DBLAST_H
+#define DBLAST_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DBL_VTILE 128
+
+typedef enum {
+  DBL_OK = 0,
+  DBL_EINVAL = 1,      /* null pointer, negative temperature, bad Kp, unknown op/dtype */
+  DBL_ESHAPE = 2,      /* a dimension outside the supported range */
+  DBL_EDTYPE = 3,      /* unsupported element type */
+  DBL_EWORKSPACE = 4,  /* workspace missing, too small or misaligned */
+  DBL_EHIP = 5         /* a HIP runtime call or kernel launch failed */
+} dbl_status;
+
+typedef enum { DBL_F32 = 0, DBL_BF16 = 1 } dbl_dtype;
+
+typedef enum {
+  DBL_OP_HEAD = 0,
+  DBL_OP_SAMPLE = 1,
+  DBL_OP_VERIFY = 2,
+  DBL_OP_EXPECTED_LEN = 3
+} dbl_op;
+
+typedef struct {
+  int64_t B, K, R, d, V;
+} dbl_shape;
+
+/* Tile width of the two-level log-probability form (128). */
+int dbl_vtile(void);
+
+/* ceil(V / 128): columns of `lmass`. */
+int64_t dbl_ntiles(int64_t V);
+
+/* Workspace bytes needed by `op` at `shape` (0 when the op needs none, SIZE_MAX if invalid). */
+size_t dbl_workspace_bytes(int op, dbl_shape shape);
+
+/* Static description of a status code. */
+const char* dbl_status_string(int status);
+
+/* Message describing the calling thread's last non-OK status ("" if none). */
+const char* dbl_last_error(void);
+
+/*
+ * dbl_head_logprobs - branch log-probabilities q_k(. | y, z) for every row (Sec.
+ * "Architecture": each branch hidden state goes through the reused target LM head; q is the
+ * softmax of the logits).
+ *
+ *   logit[m, v] = sum_j h[m*d + j] * w[v*d + j],   m < M = B*K*R, v < V
+ *
+ * in fp32 accumulation, written in the two-level form above; logits are never stored.
+ *   dt     DBL_BF16 (bf16 h and w, MFMA path) or DBL_F32 (fp32 h and w)
+ *   h      [B, K, R, d] row-major, element type dt: branch hidden states h_{k,z}
+ *   w      [V, d] row-major (the lm_head.weight layout; the math weight is w^T), type dt
+ *   tls    out [M, V] fp32      lmass  out [M, nT] fp32      lse  out [M] fp32
+ *   ws     workspace of dbl_workspace_bytes(DBL_OP_HEAD, shape) bytes (may be 0 and NULL)
+ * Errors: DBL_EINVAL for null pointers, DBL_EDTYPE for other dt, DBL_ESHAPE when d % 8 != 0
+ * or a dimension is out of range.
+ */
+dbl_status dbl_head_logprobs(dbl_shape shape, int dt, const void* h, const void* w, float* tls,
+                             float* lmass, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * dbl_sample_block - draw one block per sequence from the latent mixture (Sec. "Dependent
+ * Block Drafting and Verification": first a category from the prior, then every position in
+ * parallel from that branch). The prior is q_{Z_T}(z) = softmax(prior_logits[b, :] / z_temp)
+ * (Sec. "Drafter sampling during inference"); z_temp = 0 selects the highest-prior category
+ * (lowest index on ties).
+ *   tls, lmass, lse   the head output for this batch (shape.d is unused)
+ *   prior_logits      [B, R] fp32 category logits l_z(y)
+ *   z_temp            category temperature Z_T >= 0
+ *   seed, step        Philox key and step counter; seq_offset + b is block b's sequence index
+ *   z_out  out [B] int32 drawn category;  x_out  out [B, K] int32 drafted tokens
+ * A row whose quantised probabilities are all zero yields token -1.
+ * Errors: DBL_EINVAL for null pointers or z_temp < 0 or NaN; DBL_EWORKSPACE; DBL_ESHAPE.
+ */
+dbl_status dbl_sample_block(dbl_shape shape, const float* tls, const float* lmass,
+                            const float* lse, const float* prior_logits, float z_temp,
+                            uint64_t seed, uint64_t step, int64_t seq_offset, int32_t* z_out,
+                            int32_t* x_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * dbl_verify_block - stochastic verification of drafted blocks with the prefix-marginalised
+ * conditional q_k(v | x_<k) = sum_z w_{k,z} q_k(v | z), w_{k,z} proportional to
+ * q_{Z_T}(z) prod_{j<k} q_j(x_j | z) (Eqs. dep-conditional, category-posterior,
+ * dep-next-token-distribution). Position k is accepted with probability
+ * min(1, p_k(x_k) / q_k(x_k | x_<k)) (Eq. accept-prob) while all earlier positions were; at
+ * the first rejection the replacement is drawn from norm(max(p_k - q_k, 0)) (from p_k itself
+ * if that residual has no quantised mass); when all K are accepted and Kp = K + 1 a bonus
+ * token is drawn from p_K (Algorithm "Greedy-Branch Dependent Speculative Verification").
+ * The verifier does not take the drafted category: it uses the marginal conditional.
+ *   x            [B, K] int32 drafted tokens; ids outside [0, V) count as zero-probability
+ *   logp         [B, Kp, V] fp32 target log-probabilities p_k(.) (may hold -inf)
+ *   Kp           K or K + 1 (the extra row feeds the bonus token)
+ *   n_accept     out [B] int32 accepted positions (0..K)
+ *   next_token   out [B] int32 residual or bonus token; -1 when all K are accepted and Kp = K
+ *   accept_mass  out [B, K] fp32 or NULL: beta_k = sum_v min(p_k(v), q_k(v | x_<k)) along the
+ *                draft, every k
+ *   al_expected  out [B] fp32 or NULL: AL_b(x) = sum_i prod_{j<=i} A_j (Eq. acceptance-length)
+ *   exp_len      out [B] fp32 or NULL: E = sum_i prod_{j<=i} beta_j along the draft
+ * Errors: as dbl_sample_block, plus DBL_EINVAL for Kp not in {K, K + 1}.
+ */
+dbl_status dbl_verify_block(dbl_shape shape, const float* tls, const float* lmass,
+                            const float* lse, const float* prior_logits, float z_temp,
+                            const int32_t* x, const float* logp, int64_t Kp, uint64_t seed,
+                            uint64_t step, int64_t seq_offset, int32_t* n_accept,
+                            int32_t* next_token, float* accept_mass, float* al_expected,
+                            float* exp_len, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * dbl_expected_len - the expected-accepted-length reduction that the acceptance-oriented
+ * objective targets (Sec. "Acceptance-Oriented Training"): along a given trajectory x (for
+ * example one drawn from the target), beta_k = sum_v min(p_k(v), q_k(v | x_<k)) with the
+ * prefix-marginalised conditional, and E = sum_i prod_{j<=i} beta_j. Forward only.
+ *   x       [B, K] int32 conditioning trajectory (ids outside [0, V) count as zero-probability)
+ *   logp    [B, K, V] fp32 target log-probabilities
+ *   beta    out [B, K] fp32 or NULL;  exp_len  out [B] fp32
+ * Errors: as dbl_sample_block.
+ */
+dbl_status dbl_expected_len(dbl_shape shape, const float* tls, const float* lmass,
+                            const float* lse, const float* prior_logits, float z_temp,
+                            const int32_t* x, const float* logp, float* beta, float* exp_len,
+                            void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DBLAST_H */

@@ -1,0 +1,263 @@
+// C ABI of the DBLast library (declared in include/dblast.h): argument validation,
+// workspace layout and status mapping around the kernel launchers.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <cstdio>
+#include <string>
+
+#include "../../include/dblast.h"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dbl_status fail(dbl_status s, const std::string& msg) {
+  g_last_error = std::string(dbl_status_string(s)) + ": " + msg;
+  return s;
+}
+
+dbl_status ok() { return DBL_OK; }
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+
+int64_t ntiles(int64_t V) { return (V + DBL_VTILE - 1) / DBL_VTILE; }
+
+// Shape checks shared by every call.
+dbl_status check_shape(const dbl_shape& s, bool need_d) {
+  if (s.B < 0) return fail(DBL_ESHAPE, "B must be >= 0");
+  if (s.K < 1 || s.R < 1 || s.V < 1) return fail(DBL_ESHAPE, "K, R and V must be >= 1");
+  if (s.R > dbl::kMaxR) return fail(DBL_ESHAPE, "R must be <= 64");
+  if (s.V >= (int64_t(1) << 24)) return fail(DBL_ESHAPE, "V must be < 2^24");
+  if (s.K > (int64_t(1) << 20)) return fail(DBL_ESHAPE, "K must be <= 2^20");
+  if (need_d && (s.d < 1 || s.d > (int64_t(1) << 30)))
+    return fail(DBL_ESHAPE, "d must be in [1, 2^30]");
+  const double rows = static_cast<double>(s.B) * s.K * s.R;
+  if (rows * static_cast<double>(s.V) >= 4.0e18) return fail(DBL_ESHAPE, "B*K*R*V too large");
+  return ok();
+}
+
+struct WsLayout {
+  size_t total = 0;
+  size_t off[4] = {0, 0, 0, 0};
+};
+
+WsLayout layout(int op, const dbl_shape& s) {
+  WsLayout L;
+  const size_t B = static_cast<size_t>(s.B), K = static_cast<size_t>(s.K);
+  const size_t R = static_cast<size_t>(s.R);
+  const size_t nT = static_cast<size_t>(ntiles(s.V));
+  const size_t nchunk = static_cast<size_t>(dbl::n_chunks(static_cast<int>(nT)));
+  size_t sizes[4] = {0, 0, 0, 0};
+  int n = 0;
+  switch (op) {
+    case DBL_OP_HEAD:
+      n = 0;
+      break;
+    case DBL_OP_SAMPLE:
+      sizes[0] = B * K * nT * sizeof(uint64_t);
+      n = 1;
+      break;
+    case DBL_OP_VERIFY:
+      sizes[0] = B * K * R * sizeof(double);
+      sizes[1] = B * K * nchunk * sizeof(float);
+      sizes[2] = B * nT * sizeof(uint64_t);
+      sizes[3] = B * nT * sizeof(uint64_t);
+      n = 4;
+      break;
+    case DBL_OP_EXPECTED_LEN:
+      sizes[0] = B * K * R * sizeof(double);
+      sizes[1] = B * K * nchunk * sizeof(float);
+      n = 2;
+      break;
+    default:
+      L.total = SIZE_MAX;
+      return L;
+  }
+  size_t at = 0;
+  for (int i = 0; i < n; ++i) {
+    L.off[i] = at;
+    at += align_up(sizes[i]);
+  }
+  L.total = at;
+  return L;
+}
+
+dbl_status check_ws(int op, const dbl_shape& s, void* ws, size_t ws_bytes, WsLayout* out) {
+  *out = layout(op, s);
+  if (out->total == 0) return ok();
+  if (ws == nullptr) return fail(DBL_EWORKSPACE, "workspace pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+    return fail(DBL_EWORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < out->total)
+    return fail(DBL_EWORKSPACE, "workspace has " + std::to_string(ws_bytes) + " bytes, needs " +
+                                    std::to_string(out->total));
+  return ok();
+}
+
+dbl_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(DBL_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+dbl::BlockArgs block_args(const dbl_shape& s, const float* tls, const float* lmass,
+                          const float* lse, const float* prior, float z_temp, uint64_t seed,
+                          uint64_t step, int64_t seq_offset) {
+  dbl::BlockArgs a;
+  a.B = s.B;
+  a.K = s.K;
+  a.R = s.R;
+  a.V = s.V;
+  a.nT = static_cast<int>(ntiles(s.V));
+  a.tls = tls;
+  a.lmass = lmass;
+  a.lse = lse;
+  a.prior = prior;
+  a.z_temp = z_temp;
+  a.seed = seed;
+  a.step = step;
+  a.seq_offset = seq_offset;
+  return a;
+}
+
+dbl_status check_block_inputs(const dbl_shape& s, const float* tls, const float* lmass,
+                              const float* lse, const float* prior, float z_temp) {
+  if (dbl_status st = check_shape(s, false)) return st;
+  if (!tls || !lmass || !lse || !prior) return fail(DBL_EINVAL, "NULL input pointer");
+  if (!(z_temp >= 0.0f) || isinf(z_temp))
+    return fail(DBL_EINVAL, "z_temp must be finite and >= 0");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int dbl_vtile(void) { return DBL_VTILE; }
+
+int64_t dbl_ntiles(int64_t V) { return V < 1 ? 0 : ntiles(V); }
+
+size_t dbl_workspace_bytes(int op, dbl_shape shape) {
+  if (check_shape(shape, op == DBL_OP_HEAD) != DBL_OK) return SIZE_MAX;
+  return layout(op, shape).total;
+}
+
+const char* dbl_status_string(int status) {
+  switch (status) {
+    case DBL_OK: return "DBL_OK";
+    case DBL_EINVAL: return "DBL_EINVAL";
+    case DBL_ESHAPE: return "DBL_ESHAPE";
+    case DBL_EDTYPE: return "DBL_EDTYPE";
+    case DBL_EWORKSPACE: return "DBL_EWORKSPACE";
+    case DBL_EHIP: return "DBL_EHIP";
+    default: return "DBL_UNKNOWN";
+  }
+}
+
+const char* dbl_last_error(void) { return g_last_error.c_str(); }
+
+dbl_status dbl_head_logprobs(dbl_shape s, int dt, const void* h, const void* w, float* tls,
+                             float* lmass, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  if (dbl_status st = check_shape(s, true)) return st;
+  if (dt != DBL_F32 && dt != DBL_BF16) return fail(DBL_EDTYPE, "dtype must be DBL_F32 or DBL_BF16");
+  if (dt == DBL_BF16 && s.d % 8 != 0) return fail(DBL_ESHAPE, "bf16 head needs d % 8 == 0");
+  if (!h || !w || !tls || !lmass || !lse) return fail(DBL_EINVAL, "NULL pointer");
+  WsLayout L;
+  if (dbl_status st = check_ws(DBL_OP_HEAD, s, ws, ws_bytes, &L)) return st;
+  if (s.B == 0) return ok();
+  dbl::HeadArgs a;
+  a.M = s.B * s.K * s.R;
+  a.V = s.V;
+  a.d = static_cast<int>(s.d);
+  a.dtype_bf16 = dt == DBL_BF16;
+  a.h = h;
+  a.w = w;
+  a.tls = tls;
+  a.lmass = lmass;
+  a.lse = lse;
+  return hip_status(dbl::launch_head(a, static_cast<hipStream_t>(stream)), "head launch");
+}
+
+dbl_status dbl_sample_block(dbl_shape s, const float* tls, const float* lmass,
+                            const float* lse, const float* prior_logits, float z_temp,
+                            uint64_t seed, uint64_t step, int64_t seq_offset, int32_t* z_out,
+                            int32_t* x_out, void* ws, size_t ws_bytes, void* stream) {
+  if (dbl_status st = check_block_inputs(s, tls, lmass, lse, prior_logits, z_temp)) return st;
+  if (!z_out || !x_out) return fail(DBL_EINVAL, "NULL output pointer");
+  WsLayout L;
+  if (dbl_status st = check_ws(DBL_OP_SAMPLE, s, ws, ws_bytes, &L)) return st;
+  if (s.B == 0) return ok();
+  dbl::SampleArgs a;
+  a.blk = block_args(s, tls, lmass, lse, prior_logits, z_temp, seed, step, seq_offset);
+  a.z_out = z_out;
+  a.x_out = x_out;
+  a.tilesum = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + L.off[0]);
+  return hip_status(dbl::launch_sample(a, static_cast<hipStream_t>(stream)), "sample launch");
+}
+
+dbl_status dbl_verify_block(dbl_shape s, const float* tls, const float* lmass,
+                            const float* lse, const float* prior_logits, float z_temp,
+                            const int32_t* x, const float* logp, int64_t Kp, uint64_t seed,
+                            uint64_t step, int64_t seq_offset, int32_t* n_accept,
+                            int32_t* next_token, float* accept_mass, float* al_expected,
+                            float* exp_len, void* ws, size_t ws_bytes, void* stream) {
+  if (dbl_status st = check_block_inputs(s, tls, lmass, lse, prior_logits, z_temp)) return st;
+  if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
+  if (!n_accept || !next_token) return fail(DBL_EINVAL, "NULL output pointer");
+  if (Kp != s.K && Kp != s.K + 1) return fail(DBL_EINVAL, "Kp must be K or K + 1");
+  WsLayout L;
+  if (dbl_status st = check_ws(DBL_OP_VERIFY, s, ws, ws_bytes, &L)) return st;
+  if (s.B == 0) return ok();
+  char* base = static_cast<char*>(ws);
+  dbl::VerifyArgs a;
+  a.blk = block_args(s, tls, lmass, lse, prior_logits, z_temp, seed, step, seq_offset);
+  a.x = x;
+  a.logp = logp;
+  a.Kp = Kp;
+  a.trajectory = false;
+  a.n_accept = n_accept;
+  a.next_token = next_token;
+  a.beta = accept_mass;
+  a.al = al_expected;
+  a.exp_len = exp_len;
+  a.wpost = reinterpret_cast<double*>(base + L.off[0]);
+  a.beta_part = reinterpret_cast<float*>(base + L.off[1]);
+  a.res_tiles = reinterpret_cast<uint64_t*>(base + L.off[2]);
+  a.p_tiles = reinterpret_cast<uint64_t*>(base + L.off[3]);
+  return hip_status(dbl::launch_verify(a, static_cast<hipStream_t>(stream)), "verify launch");
+}
+
+dbl_status dbl_expected_len(dbl_shape s, const float* tls, const float* lmass,
+                            const float* lse, const float* prior_logits, float z_temp,
+                            const int32_t* x, const float* logp, float* beta, float* exp_len,
+                            void* ws, size_t ws_bytes, void* stream) {
+  if (dbl_status st = check_block_inputs(s, tls, lmass, lse, prior_logits, z_temp)) return st;
+  if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
+  if (!exp_len) return fail(DBL_EINVAL, "NULL output pointer");
+  WsLayout L;
+  if (dbl_status st = check_ws(DBL_OP_EXPECTED_LEN, s, ws, ws_bytes, &L)) return st;
+  if (s.B == 0) return ok();
+  char* base = static_cast<char*>(ws);
+  dbl::VerifyArgs a;
+  a.blk = block_args(s, tls, lmass, lse, prior_logits, z_temp, 0, 0, 0);
+  a.x = x;
+  a.logp = logp;
+  a.Kp = s.K;
+  a.trajectory = true;
+  a.n_accept = nullptr;
+  a.next_token = nullptr;
+  a.beta = beta;
+  a.al = nullptr;
+  a.exp_len = exp_len;
+  a.wpost = reinterpret_cast<double*>(base + L.off[0]);
+  a.beta_part = reinterpret_cast<float*>(base + L.off[1]);
+  a.res_tiles = nullptr;
+  a.p_tiles = nullptr;
+  return hip_status(dbl::launch_verify(a, static_cast<hipStream_t>(stream)),
+                    "expected_len launch");
+}
+
+}  // extern "C"

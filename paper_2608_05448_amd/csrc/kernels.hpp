@@ -1,0 +1,67 @@
+// Launch interfaces between the C ABI (abi.hip) and the kernels. Internal to the library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dbl {
+
+constexpr int kTile = 128;            // vocabulary tile of the two-level log-prob form
+constexpr int kTilesPerChunk = 32;    // vocabulary tiles per workgroup in the V-streaming kernels
+constexpr int kMaxR = 64;             // categories handled by one wavefront
+
+struct HeadArgs {
+  int64_t M, V;
+  int d;
+  bool dtype_bf16;
+  const void* h;
+  const void* w;
+  float* tls;
+  float* lmass;
+  float* lse;
+};
+
+// The branch log-probabilities and block description shared by the sampler and verifier.
+struct BlockArgs {
+  int64_t B, K, R, V;
+  int nT;
+  const float* tls;
+  const float* lmass;
+  const float* lse;
+  const float* prior;  // [B, R]
+  float z_temp;
+  uint64_t seed, step;
+  int64_t seq_offset;
+};
+
+struct SampleArgs {
+  BlockArgs blk;
+  int32_t* z_out;
+  int32_t* x_out;
+  uint64_t* tilesum;  // workspace [B*K, nT]
+};
+
+struct VerifyArgs {
+  BlockArgs blk;
+  const int32_t* x;     // [B, K]
+  const float* logp;    // [B, Kp, V]
+  int64_t Kp;
+  bool trajectory;      // expected-length mode: no accept test, no residual
+  int32_t* n_accept;    // [B] (verify only)
+  int32_t* next_token;  // [B] (verify only)
+  float* beta;          // [B, K] or null
+  float* al;            // [B] or null
+  float* exp_len;       // [B] or null
+  double* wpost;        // workspace [B, K, R]: posterior weights
+  float* beta_part;     // workspace [B*K, nchunk]
+  uint64_t* res_tiles;  // workspace [B, nT]
+  uint64_t* p_tiles;    // workspace [B, nT]
+};
+
+inline int n_chunks(int nT) { return (nT + kTilesPerChunk - 1) / kTilesPerChunk; }
+
+hipError_t launch_head(const HeadArgs& a, hipStream_t stream);
+hipError_t launch_sample(const SampleArgs& a, hipStream_t stream);
+hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
+
+}  // namespace dbl

@@ -1,0 +1,141 @@
+// Wavefront (64-lane) helpers shared by the sampler and verifier kernels. Internal.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "contract.hpp"
+#include "kernels.hpp"
+
+namespace dbl {
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ double wave_max_f64(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum_f32(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Inclusive prefix sum over the 64 lanes.
+__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t t = __shfl_up(v, o);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+// Unnormalised log prior of category z = lane (lanes >= R hold -inf): l_z / Z_T, or for
+// Z_T = 0, 0 at the lowest-index maximum of l and -inf elsewhere.
+__device__ __forceinline__ double prior_log_weight(const float* prior_row, int R, float z_temp) {
+  const int lane = lane_id();
+  const float l = lane < R ? prior_row[lane] : -INFINITY;
+  if (z_temp > 0.0f)
+    return lane < R ? static_cast<double>(l) / static_cast<double>(z_temp) : -INFINITY;
+  float mx = l;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  const uint64_t hit = __ballot(lane < R && l == mx);
+  const int top = __ffsll(static_cast<unsigned long long>(hit)) - 1;
+  return lane == top ? 0.0 : -INFINITY;
+}
+
+// w_z = exp(L_z - max L) / sum_z exp(L_z - max L), the sum taken over ascending z with each
+// addition rounded separately; every lane computes the identical sum. An all -inf row (an
+// impossible prefix) gives all-zero weights.
+__device__ __forceinline__ double normalize_weight(double L, int R) {
+  const double mx = wave_max_f64(L);
+  if (!(mx > -INFINITY)) return 0.0;
+  const double e = dexp64(__dsub_rn(L, mx));
+  double S = 0.0;
+  for (int z = 0; z < R; ++z) S = __dadd_rn(S, __shfl(e, z));
+  return e / S;
+}
+
+// The category z ~ q_{Z_T} of block b by inverse CDF on floor(w_z 2^40); all lanes agree.
+__device__ __forceinline__ int draw_category(const BlockArgs& a, int64_t b) {
+  const int lane = lane_id();
+  const int R = static_cast<int>(a.R);
+  const double w = normalize_weight(prior_log_weight(a.prior + b * a.R, R, a.z_temp), R);
+  const uint64_t qz = lane < R ? quant40d(w) : 0;
+  uint64_t Z = 0;
+  for (int z = 0; z < R; ++z) Z += __shfl(qz, z);
+  if (Z == 0) return -1;
+  const uint32_t r = draw(a.seed, kCategory, 0, static_cast<uint64_t>(a.seq_offset + b), a.step);
+  const uint64_t T = icdf_threshold(r, Z);
+  uint64_t cum = 0;
+  for (int z = 0; z < R; ++z) {
+    cum += __shfl(qz, z);
+    if (cum > T) return z;
+  }
+  return R - 1;  // unreachable: cum reaches Z > T
+}
+
+// Inverse-CDF selection over per-tile integer sums followed by an in-tile scan.
+// `tiles` holds the nT tile sums; weight(v) recomputes the integer weight of id v (v < V).
+// Returns the smallest id whose inclusive cumulative weight exceeds floor(r Z / 2^32), or -1
+// when the total weight Z is 0. Executed by one full wavefront; all lanes return the result.
+template <class WeightFn>
+__device__ __forceinline__ int select_by_tiles(const uint64_t* tiles, int nT, int64_t V,
+                                               uint32_t r, WeightFn weight) {
+  const int lane = lane_id();
+  uint64_t part = 0;
+  for (int t = lane; t < nT; t += 64) part += tiles[t];
+  const uint64_t Z = wave_sum_u64(part);
+  if (Z == 0) return -1;
+  const uint64_t T = icdf_threshold(r, Z);
+  // Find the tile holding T.
+  uint64_t running = 0;
+  int tsel = -1;
+  uint64_t before = 0;
+  for (int t0 = 0; t0 < nT; t0 += 64) {
+    const int t = t0 + lane;
+    const uint64_t val = t < nT ? tiles[t] : 0;
+    const uint64_t incl = wave_incl_scan_u64(val) + running;
+    const uint64_t hit = __ballot(t < nT && incl > T);
+    if (hit) {
+      const int l = __ffsll(static_cast<unsigned long long>(hit)) - 1;
+      tsel = t0 + l;
+      before = __shfl(incl - val, l);
+      break;
+    }
+    running = __shfl(incl, 63);
+  }
+  if (tsel < 0) return -1;  // unreachable for consistent tile sums
+  // In-tile scan: lane holds ids 128 tsel + 2 lane + {0, 1}.
+  const int64_t v0 = static_cast<int64_t>(tsel) * kTile + 2 * lane;
+  const uint64_t q0 = v0 < V ? weight(v0) : 0;
+  const uint64_t q1 = v0 + 1 < V ? weight(v0 + 1) : 0;
+  const uint64_t incl = wave_incl_scan_u64(q0 + q1);
+  const uint64_t c0 = before + incl - q1;  // cumulative through id v0
+  const uint64_t c1 = before + incl;       // cumulative through id v0 + 1
+  const bool h0 = c0 > T, h1 = c1 > T;
+  const uint64_t hit = __ballot(h0 || h1);
+  if (!hit) return -1;  // unreachable for consistent tile sums
+  const int l = __ffsll(static_cast<unsigned long long>(hit)) - 1;
+  const int pick0 = __shfl(static_cast<int>(h0), l);
+  return static_cast<int>(static_cast<int64_t>(tsel) * kTile + 2 * l + (pick0 ? 0 : 1));
+}
+
+}  // namespace dbl

@@ -1,0 +1,144 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared symbol, sizes its
+workspace, and rejects invalid arguments before any GPU work (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_05448_amd import dblast as D
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dblast.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dbl_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(D.LIB_PATH):
+        pytest.fail("libdblast.so is not built (run `python -m paper_2608_05448_amd.build`)")
+    return D.load()
+
+
+def test_every_declared_symbol_is_exported_and_bound(lib):
+    declared = _declared_functions()
+    assert set(declared) == set(D.EXPORTED), (declared, D.EXPORTED)
+    for name in declared:
+        assert getattr(lib, name) is not None
+
+
+def test_constants_and_status_strings(lib):
+    assert lib.dbl_vtile() == 128
+    assert lib.dbl_ntiles(151936) == 1187
+    assert lib.dbl_ntiles(129) == 2
+    assert lib.dbl_ntiles(0) == 0
+    for s, name in enumerate(["DBL_OK", "DBL_EINVAL", "DBL_ESHAPE", "DBL_EDTYPE",
+                              "DBL_EWORKSPACE", "DBL_EHIP"]):
+        assert lib.dbl_status_string(s).decode() == name
+    assert lib.dbl_status_string(99).decode() == "DBL_UNKNOWN"
+
+
+def test_workspace_sizes(lib):
+    S = D.Shape
+    SIZE_MAX = ctypes.c_size_t(-1).value
+    assert lib.dbl_workspace_bytes(D.DBL_OP_HEAD, S(16, 16, 8, 4096, 151936)) == 0
+    # Sample: one uint64 per (position, tile).
+    assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, S(16, 16, 8, 0, 151936)) == \
+        -(-16 * 16 * 1187 * 8 // 256) * 256
+    v = lib.dbl_workspace_bytes(D.DBL_OP_VERIFY, S(16, 16, 8, 0, 151936))
+    e = lib.dbl_workspace_bytes(D.DBL_OP_EXPECTED_LEN, S(16, 16, 8, 0, 151936))
+    assert v > e > 0 and v % 256 == 0 and e % 256 == 0
+    assert lib.dbl_workspace_bytes(7, S(1, 1, 1, 8, 8)) == SIZE_MAX
+    assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, S(1, 1, 65, 8, 8)) == SIZE_MAX
+    assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, S(0, 4, 2, 8, 256)) == 0
+
+
+def _fake(n=1):
+    # Non-null dummy addresses. Every call made with them below is invalid in some other
+    # argument and must be rejected by host validation before anything is launched.
+    return [ctypes.c_void_p(0x1000 * (i + 1)) for i in range(n)]
+
+
+def _err(lib):
+    return lib.dbl_last_error().decode()
+
+
+def test_head_validation(lib):
+    S = D.Shape
+    h, w, t, lm, ls = _fake(5)
+    null = ctypes.c_void_p(None)
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 60, 256), D.DBL_BF16, h, w, t, lm, ls, null, 0,
+                                 null) == D.DBL_ESHAPE
+    assert "d % 8" in _err(lib)
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 256), 7, h, w, t, lm, ls, null, 0,
+                                 null) == D.DBL_EDTYPE
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 256), D.DBL_F32, null, w, t, lm, ls, null, 0,
+                                 null) == D.DBL_EINVAL
+    assert lib.dbl_head_logprobs(S(1, 0, 2, 64, 256), D.DBL_F32, h, w, t, lm, ls, null, 0,
+                                 null) == D.DBL_ESHAPE
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 1 << 24), D.DBL_F32, h, w, t, lm, ls, null, 0,
+                                 null) == D.DBL_ESHAPE
+    assert lib.dbl_head_logprobs(S(-1, 4, 2, 64, 256), D.DBL_F32, h, w, t, lm, ls, null, 0,
+                                 null) == D.DBL_ESHAPE
+
+
+def test_sample_and_verify_validation(lib):
+    S = D.Shape
+    p = _fake(12)
+    null = ctypes.c_void_p(None)
+    shape = S(2, 4, 3, 0, 300)
+    ws_need = lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, shape)
+    aligned = ctypes.c_void_p(0x100000)
+    # Negative and NaN temperatures.
+    for zt in (-0.5, float("nan"), float("inf")):
+        assert lib.dbl_sample_block(shape, p[0], p[1], p[2], p[3], zt, 0, 0, 0, p[4], p[5],
+                                    aligned, ws_need, null) == D.DBL_EINVAL
+    # Workspace: missing, too small, misaligned.
+    assert lib.dbl_sample_block(shape, p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4], p[5],
+                                null, ws_need, null) == D.DBL_EWORKSPACE
+    assert lib.dbl_sample_block(shape, p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4], p[5],
+                                aligned, ws_need - 1, null) == D.DBL_EWORKSPACE
+    assert lib.dbl_sample_block(shape, p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4], p[5],
+                                ctypes.c_void_p(0x100010), ws_need, null) == D.DBL_EWORKSPACE
+    assert "256-byte" in _err(lib)
+    # Too many categories.
+    assert lib.dbl_sample_block(S(2, 4, 65, 0, 300), p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4],
+                                p[5], aligned, 1 << 30, null) == D.DBL_ESHAPE
+    vws = lib.dbl_workspace_bytes(D.DBL_OP_VERIFY, shape)
+    # Kp must be K or K + 1.
+    for kp in (3, 6):
+        assert lib.dbl_verify_block(shape, p[0], p[1], p[2], p[3], 1.0, p[4], p[5], kp, 0, 0, 0,
+                                    p[6], p[7], null, null, null, aligned, vws,
+                                    null) == D.DBL_EINVAL
+    assert lib.dbl_verify_block(shape, p[0], p[1], p[2], p[3], 1.0, p[4], p[5], 4, 0, 0, 0,
+                                null, p[7], null, null, null, aligned, vws, null) == D.DBL_EINVAL
+    ews = lib.dbl_workspace_bytes(D.DBL_OP_EXPECTED_LEN, shape)
+    assert lib.dbl_expected_len(shape, p[0], p[1], p[2], p[3], 1.0, p[4], p[5], null, null,
+                                aligned, ews, null) == D.DBL_EINVAL
+
+
+def test_empty_batch_is_a_no_op(lib):
+    S = D.Shape
+    p = _fake(8)
+    null = ctypes.c_void_p(None)
+    assert lib.dbl_sample_block(S(0, 4, 2, 0, 256), p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4],
+                                p[5], null, 0, null) == D.DBL_OK
+    assert lib.dbl_verify_block(S(0, 4, 2, 0, 256), p[0], p[1], p[2], p[3], 1.0, p[4], p[5], 4,
+                                0, 0, 0, p[6], p[7], null, null, null, null, 0, null) == D.DBL_OK
+    assert lib.dbl_expected_len(S(0, 4, 2, 0, 256), p[0], p[1], p[2], p[3], 1.0, p[4], p[5],
+                                null, p[6], null, 0, null) == D.DBL_OK
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    saved = D._lib
+    D._lib = None
+    try:
+        with pytest.raises(RuntimeError, match="not built"):
+            D.load(str(tmp_path / "missing.so"))
+    finally:
+        D._lib = saved

@@ -1,0 +1,109 @@
+"""GPU parity of dbl_head_logprobs against the oracle head (binary64 GEMM + log-softmax).
+
+Tolerances: 2e-5 absolute on log-probabilities for fp32 inputs and 2e-3 for bf16 inputs with
+fp32 accumulation (both sides read the identical bf16 values).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from cases import flat_from_factored, np32
+from oracle import head as OH
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(h, w):
+    from paper_2608_05448_amd import dblast as D
+    out = D.dbl_head_logprobs(h.cuda(), w.cuda())
+    torch.cuda.synchronize()
+    return [t.cpu().numpy() for t in out]
+
+
+def _check(h, w, tol, label):
+    B, K, R, d = h.shape
+    V = w.shape[0]
+    print(f"[head] {label} B={B} K={K} R={R} d={d} V={V} dtype={h.dtype}", flush=True)
+    tls, lmass, lse = _run(h, w)
+    hh, ww = np32(h).reshape(-1, d), np32(w)
+    ref = OH.head_logq(hh, ww)
+    got = flat_from_factored(tls.reshape(-1, V), lmass.reshape(-1, lmass.shape[-1]),
+                             lse.reshape(-1)).astype(np.float64)
+    err = np.max(np.abs(got - ref))
+    print(f"[head] {label} max |log q error| = {err:.3e}", flush=True)
+    assert err < tol
+    # The factored parts individually.
+    r_tls, r_lm, r_lse = OH.factor_logits(OH.head_logits(hh, ww))
+    assert np.max(np.abs(tls.reshape(-1, V) - r_tls)) < tol
+    assert np.max(np.abs(lmass.reshape(-1, lmass.shape[-1]) - r_lm)) < tol
+    assert np.max(np.abs(lse.reshape(-1) - r_lse)) < tol
+
+
+def test_head_fp32_tiny_workload():
+    wl = synth.WORKLOADS["tiny"]
+    _check(synth.make_h(wl), synth.make_w(wl), 2e-5, "tiny")
+
+
+@pytest.mark.parametrize("B,K,R,d,V", [
+    (3, 2, 5, 100, 1000),    # d not a multiple of 8 (fp32 path allows it), ragged last tile
+    (1, 1, 1, 1, 1),         # smallest problem
+    (2, 3, 7, 40, 129),      # one id in the last tile
+])
+def test_head_fp32_ragged(B, K, R, d, V):
+    h = synth.make_uniform_logits((B, K, R, d), 11).to(torch.float32)
+    w = (synth.make_uniform_logits((V, d), 12) / math.sqrt(d)).to(torch.float32)
+    _check(h, w, 2e-5, "fp32-ragged")
+
+
+@pytest.mark.parametrize("B,K,R,d,V", [
+    (3, 2, 5, 136, 1000),    # hidden size not a multiple of the 32-wide K step; ragged tiles
+    (2, 10, 15, 512, 5000),  # several branch-row and vocabulary tiles, ragged on both
+    (1, 4, 5, 64, 1001),     # V % 4 != 0: scalar stores
+    (1, 1, 5, 8, 77),        # fewer ids than one tile
+    (4, 16, 8, 256, 2048),   # exact tile multiples
+])
+def test_head_bf16_ragged(B, K, R, d, V):
+    h = synth.make_uniform_logits((B, K, R, d), 21).to(torch.bfloat16)
+    w = (synth.make_uniform_logits((V, d), 22) * 0.05).to(torch.bfloat16)
+    _check(h, w, 2e-3, "bf16-ragged")
+
+
+def test_head_bf16_qwen3_4b_sampled_rows():
+    """Full Qwen3-4B-shaped head in the benchmark's launch; the oracle checks sampled rows and
+    tile-level identities that hold for every row."""
+    _full_size_rows("qwen3_4b", rows=(0, 517, 1023))
+
+
+def test_head_bf16_qwen3_8b_sampled_rows():
+    _full_size_rows("qwen3_8b", rows=(0, 1111, 2047))
+
+
+def _full_size_rows(name, rows):
+    from paper_2608_05448_amd import dblast as D
+    wl = synth.WORKLOADS[name]
+    print(f"[head] full-size {name} M={wl.M} d={wl.d} V={wl.V}", flush=True)
+    h = synth.make_h(wl, "cuda")
+    w = synth.make_w(wl, "cuda")
+    tls, lmass, lse = D.dbl_head_logprobs(h, w)
+    torch.cuda.synchronize()
+    M, V, nT = wl.M, wl.V, OH.n_tiles(wl.V)
+    t2 = tls.view(M, V)
+    # Identities at every row: each tile's probabilities sum to 1, tile masses sum to 1.
+    tile_sums = torch.exp(t2.view(M, nT, 128).double()).sum(-1)   # V = 1187 * 128 exactly
+    assert torch.max(torch.abs(tile_sums - 1.0)).item() < 1e-5
+    mass = torch.exp((lmass.view(M, nT) - lse.view(M, 1)).double()).sum(-1)
+    assert torch.max(torch.abs(mass - 1.0)).item() < 1e-5
+    assert torch.max(t2).item() <= 1e-6
+    # Sampled rows against the oracle.
+    hh = np32(h.view(M, wl.d)[list(rows)])
+    ww = np32(w)
+    r_tls, r_lm, r_lse = OH.head_factored(hh, ww, v_chunk=8192)
+    ref = flat_from_factored(r_tls, r_lm, r_lse).astype(np.float64)
+    got = flat_from_factored(t2[list(rows)].cpu().numpy(), lmass.view(M, nT)[list(rows)].cpu().numpy(),
+                             lse.view(M)[list(rows)].cpu().numpy()).astype(np.float64)
+    err = np.max(np.abs(got - ref))
+    print(f"[head] full-size {name} sampled rows max |log q error| = {err:.3e}", flush=True)
+    assert err < 2e-3
