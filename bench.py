@@ -1,0 +1,239 @@
+"""Throughput of the DBLast head + block draw + verification on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen3_8b]
+                    [--temperature T] [--no-cpu-baseline] [--copy-calibration BYTES]
+
+One step is one pass of the whole hot path over one batch of synthetic inputs already resident
+in HBM: dbl_head_logprobs (bf16 head GEMM + per-tile log-softmax), dbl_sample_block (category
+and token draw) and dbl_verify_block (posterior, accept test, residual/bonus draw, acceptance
+masses, AL_b and E). The Philox step counter advances every step. Prints one JSON line.
+
+The metric is verified block positions per second, B*K / step time. The roofline entry is for
+the dominant kernel, the head GEMM: 2*M*d*V flops per launch over its average launch time,
+measured with HIP events on the stream the library launches on, against MI355X's dense bf16
+peak. The CPU baseline times the oracle (binary64 NumPy) on a bounded sample of the same
+workload on this machine's host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "verified block positions/sec at Qwen3-8B head shape; head-GEMM MFMA % of peak"
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "head_bf16_qwen3_8b_traffic.json")
+HEAD_SOURCE = os.path.join(ROOT, "paper_2608_05448_amd", "csrc", "head.hip")
+
+
+def _head_source_hash() -> str:
+    with open(HEAD_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def _traffic(workload: str):
+    """HBM bytes per head launch from the committed rocprofv3 counter summary, or None when it
+    is missing or was taken on a different head kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("head_source_sha256_16") != _head_source_hash() or rec.get("workload") != workload:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def _cpu_baseline(wl, h, w, ell, logp, budget_s: float):
+    """The oracle on as many whole blocks as fit the time budget (at least one)."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import head as OH
+    from oracle import mixture as MX
+
+    ww = w.float().cpu().numpy()
+    hh = h.float().cpu().numpy()
+    ee = ell.cpu().numpy()
+    lp = logp.cpu().numpy()
+    K, R, d, V = wl.K, wl.R, wl.d, wl.V
+    t0 = time.perf_counter()
+    done = 0
+    for b in range(wl.B):
+        tls, lm, ls = OH.head_factored(hh[b].reshape(K * R, d), ww, v_chunk=8192)
+        lq = OH.flat_logq(tls, lm, ls).reshape(1, K, R, V)
+        seq = np.array([b])
+        _, x = MX.sample_blocks(lq, ee[b:b + 1], wl.z_temp, wl.philox_seed, 0, seq)
+        MX.verify_blocks(lq, ee[b:b + 1], wl.z_temp, x, lp[b:b + 1], wl.philox_seed, 0, seq)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    cores = len(os.sched_getaffinity(0))
+    return {"value": done * K / el, "unit": "positions/s", "cores": min(threads, cores),
+            "kind": "oracle",
+            "sample": f"{done} of {wl.B} blocks ({done * K} positions): binary64 head, block draw "
+                      f"and verification, {el:.1f} s on the host"}
+
+
+def _copy_calibration(nbytes: int):
+    """A plain device copy of known size, for scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    n = nbytes // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen3_8b")
+    ap.add_argument("--temperature", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-calibration", type=int, default=0)
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the hot "
+              "path shards over blocks with no exchange; see the multi-GPU design notes)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import synth
+    from paper_2608_05448_amd import dblast as D
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    if args.copy_calibration:
+        _copy_calibration(args.copy_calibration)
+        return 0
+
+    wl = synth.WORKLOADS[args.workload]
+    if args.temperature is not None:
+        wl = wl.replace(temperature=args.temperature)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    D.load()
+
+    # Inputs resident in HBM before timing.
+    h = synth.make_h(wl, dev)
+    w = synth.make_w(wl, dev)
+    ell = synth.make_ell(wl, dev)
+    logp = synth.make_logp(wl, rows=wl.K + 1, device=dev)
+    B, K, R, d, V = wl.B, wl.K, wl.R, wl.d, wl.V
+    nT = D.ntiles(V)
+    tls = torch.empty((B, K, R, V), dtype=torch.float32, device=dev)
+    lmass = torch.empty((B, K, R, nT), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, K, R), dtype=torch.float32, device=dev)
+    z = torch.empty(B, dtype=torch.int32, device=dev)
+    x = torch.empty((B, K), dtype=torch.int32, device=dev)
+    vout = {"n_accept": torch.empty(B, dtype=torch.int32, device=dev),
+            "next_token": torch.empty(B, dtype=torch.int32, device=dev),
+            "accept_mass": torch.empty((B, K), dtype=torch.float32, device=dev),
+            "al_expected": torch.empty(B, dtype=torch.float32, device=dev),
+            "exp_len": torch.empty(B, dtype=torch.float32, device=dev)}
+    ws_s = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_SAMPLE, B, K, R, d, V), dtype=torch.uint8,
+                       device=dev)
+    ws_v = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_VERIFY, B, K, R, d, V), dtype=torch.uint8,
+                       device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(t, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        D.dbl_head_logprobs(h, w, tls, lmass, lse)
+        if ev is not None:
+            ev[1].record(stream)
+        D.dbl_sample_block(tls, lmass, lse, ell, z_temp=wl.z_temp, seed=wl.philox_seed, step=t,
+                           z_out=z, x_out=x, ws=ws_s)
+        if ev is not None:
+            ev[2].record(stream)
+        D.dbl_verify_block(tls, lmass, lse, ell, x, logp, z_temp=wl.z_temp, seed=wl.philox_seed,
+                           step=t, out=vout, ws=ws_v)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize(dev)
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    acc_sum = 0.0
+    torch.cuda.synchronize(dev)
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, events[i])
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t_wall
+
+    head_ms = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
+    sample_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps
+    verify_ms = sum(e[2].elapsed_time(e[3]) for e in events) / args.steps
+    step_ms = events[0][0].elapsed_time(events[-1][3]) / args.steps
+    acc_sum = float(vout["n_accept"].float().mean().item())
+    exp_len = float(vout["exp_len"].float().mean().item())
+
+    M = B * K * R
+    head_flop = 2.0 * M * d * V
+    head_tflops = head_flop / (head_ms * 1e-3) / 1e12
+    verify_bytes = B * K * (R + 1) * V * 4.0
+    sample_bytes = B * K * V * 4.0
+    traffic = _traffic(args.workload)
+
+    out = {
+        "metric": METRIC,
+        "value": B * K / (step_ms * 1e-3),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "K": K, "R": R, "d": d, "V": V,
+                   "global_batch": B, "positions_per_step": B * K,
+                   "target_temperature": wl.temperature, "z_temp": wl.z_temp,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": head_tflops, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": head_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": traffic,
+                     "kernel": "dbl_head_logprobs (head GEMM + per-tile log-softmax, LSE)"},
+        "kernels_ms": {"head": head_ms, "sample": sample_ms, "verify": verify_ms},
+        "hbm": {"verify_GBps": verify_bytes / (verify_ms * 1e-3) / 1e9,
+                "verify_frac": verify_bytes / (verify_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                "sample_GBps": sample_bytes / (sample_ms * 1e-3) / 1e9,
+                "sample_frac": sample_bytes / (sample_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
+        "quality": {"mean_n_accept": acc_sum, "mean_exp_len": exp_len},
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = _cpu_baseline(wl, h, w, ell, logp, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
