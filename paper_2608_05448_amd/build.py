@@ -38,14 +38,16 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: the DBLast library needs ROCm's hipcc to build")
 
 
-def build(verbose: bool = False, jobs: int = 4) -> str:
-    """Compile every HIP source for gfx950 and link libdblast.so; returns its path."""
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = False, jobs: int = 4, extra_flags=(), out: str = LIB,
+          build_dir: str = BUILD) -> str:
+    """Compile every HIP source for gfx950 and link the library (libdblast.so by default);
+    returns its path. ``extra_flags`` are added to every compile (e.g. tile-size macros)."""
+    os.makedirs(build_dir, exist_ok=True)
     cc = hipcc()
     procs, objs = [], []
     for src, extra in SOURCES.items():
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        cmd = [cc, *COMMON, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+        obj = os.path.join(build_dir, src.replace(".hip", ".o"))
+        cmd = [cc, *COMMON, *extra, *extra_flags, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT,
@@ -54,20 +56,20 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
         while len([p for _, p in procs if p.poll() is None]) >= jobs:
             procs[0][1].wait()
     for src, p in procs:
-        out, _ = p.communicate()
+        log, _ = p.communicate()
         if p.returncode != 0:
-            raise RuntimeError(f"hipcc failed on {src}:\n{out}")
-        if verbose and out.strip():
-            print(out)
-    tmp = LIB + ".tmp"
+            raise RuntimeError(f"hipcc failed on {src}:\n{log}")
+        if verbose and log.strip():
+            print(log)
+    tmp = out + ".tmp"
     cmd = [cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

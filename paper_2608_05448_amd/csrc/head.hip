@@ -11,6 +11,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace dbl {
@@ -21,6 +23,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kVTile = 128;
+constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
@@ -31,6 +34,81 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
   return v;
+}
+
+// Epilogue shared by the bf16 kernels. The wave holds the logits of one vocabulary tile (ids
+// v0w .. v0w + 127) for NCB * 32 branch rows. Lane l holds row m0w + 32 cb + l % 32 and, in
+// register r of row block rb, id v0w + 32 rb + 8 (r / 4) + 4 (l / 32) + r % 4. For each row:
+// tile max and sum of exponentials in registers plus one cross-half exchange, then the tile
+// log-mass and the tile-normalised log-probs are written; logits never reach memory.
+template <int NRB, int NCB>
+__device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], float* tls,
+                                                      float* lmass, int64_t M, int64_t V,
+                                                      int nT, int64_t v0w, int64_t m0w,
+                                                      int lane, int vec4) {
+  const int half = lane >> 5;
+  const int t = static_cast<int>(v0w / kVTile);
+  const int vlim = static_cast<int>(V - v0w < kVTile ? V - v0w : kVTile);  // ids in this tile
+  const bool full = vlim == kVTile;
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    const int64_t m = m0w + cb * 32 + (lane & 31);
+    float mx = -INFINITY;
+    float s = 0.0f;
+    if (full) {
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[rb][cb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float nb = -mx * kLog2e;
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s += __builtin_amdgcn_exp2f(fmaf(acc[rb][cb][r], kLog2e, nb));
+    } else {
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3) < vlim) mx = fmaxf(mx, acc[rb][cb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3) < vlim)
+            s += __expf(acc[rb][cb][r] - mx);
+    }
+    s += __shfl_xor(s, 32);
+    const float lm = mx + __logf(s);
+    if (m < M) {
+      if (half == 0) lmass[m * nT + t] = lm;
+      float* row = tls + m * V + v0w + 4 * half;
+      if (full && vec4) {
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            float4 o;
+            o.x = acc[rb][cb][4 * g + 0] - lm;
+            o.y = acc[rb][cb][4 * g + 1] - lm;
+            o.z = acc[rb][cb][4 * g + 2] - lm;
+            o.w = acc[rb][cb][4 * g + 3] - lm;
+            *reinterpret_cast<float4*>(row + rb * 32 + 8 * g) = o;
+          }
+      } else {
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (rb * 32 + 8 * g + 4 * half + e < vlim)
+                row[rb * 32 + 8 * g + e] = acc[rb][cb][4 * g + e] - lm;
+      }
+    }
+  }
 }
 
 // Tile configuration of the bf16 head kernel.
@@ -54,19 +132,39 @@ struct HeadCfg {
   static_assert((BV * CPR) % kThreads == 0 && (BM * CPR) % kThreads == 0, "even staging");
 };
 
-using Cfg = HeadCfg<256, 128, 32, 2, 2>;
+using Cfg = HeadCfg<256, 256, 64, 2, 2>;
 
-// Maps the hardware workgroup id to a logical tile so that consecutive logical tiles (the
-// branch-row tiles that share one vocabulary slab of w) land on the same XCD: workgroups are
-// dispatched round-robin over the 8 XCDs, each with its own L2.
+// Maps the hardware workgroup id to a logical tile id so that consecutive logical ids land on
+// the same XCD: workgroups are dispatched round-robin over the 8 XCDs, each with its own L2.
 __device__ __forceinline__ int xcd_remap(int id, int n) {
   const int q = n >> 3, rem = n & 7;
   const int x = id & 7, s = id >> 3;
   return x < rem ? x * (q + 1) + s : rem * (q + 1) + (x - rem) * q + s;
 }
 
+// Logical tile id -> (vocabulary tile, branch-row tile). Branch-row tiles are taken in groups
+// of up to kGroupM; a group sweeps every vocabulary tile before the next group starts, and
+// within a vocabulary tile the group's branch-row tiles are consecutive. The ~32 workgroups
+// resident on one XCD therefore cover about 4 vocabulary x 8 branch-row tiles: each slab of w
+// is read by up to 8 of them and each slab of h by about 4, from that XCD's L2.
+constexpr int kGroupM = 8;
+__device__ __forceinline__ void tile_of(int L, int n_vtiles, int n_mtiles, int* vt, int* mt) {
+  const int n_groups = (n_mtiles + kGroupM - 1) / kGroupM;
+  const int per_full = n_vtiles * kGroupM;
+  if (L < (n_groups - 1) * per_full) {
+    const int g = L / per_full, rem = L % per_full;
+    *vt = rem / kGroupM;
+    *mt = g * kGroupM + rem % kGroupM;
+  } else {
+    const int rem = L - (n_groups - 1) * per_full;
+    const int gl = n_mtiles - (n_groups - 1) * kGroupM;
+    *vt = rem / gl;
+    *mt = (n_groups - 1) * kGroupM + rem % gl;
+  }
+}
+
 template <class C>
-__global__ __launch_bounds__(C::kThreads, 2) void head_bf16_kernel(
+__global__ __launch_bounds__(C::kThreads, 1) void head_bf16_kernel(
     const __bf16* __restrict__ h, const __bf16* __restrict__ w, float* __restrict__ tls,
     float* __restrict__ lmass, int64_t M, int64_t V, int d, int nT, int n_mtiles, int vec4) {
   __shared__ __attribute__((aligned(16))) __bf16 As[2][C::BV * C::LDK];
@@ -78,9 +176,8 @@ __global__ __launch_bounds__(C::kThreads, 2) void head_bf16_kernel(
   const int wv = wave / C::WM;  // wave row (vocabulary)
   const int wm = wave % C::WM;  // wave column (branch rows)
 
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int mt = logical % n_mtiles;
-  const int vt = logical / n_mtiles;
+  int vt, mt;
+  tile_of(xcd_remap(blockIdx.x, gridDim.x), gridDim.x / n_mtiles, n_mtiles, &vt, &mt);
   const int64_t v0 = static_cast<int64_t>(vt) * C::BV;
   const int64_t m0 = static_cast<int64_t>(mt) * C::BM;
 
@@ -110,20 +207,25 @@ __global__ __launch_bounds__(C::kThreads, 2) void head_bf16_kernel(
   }
 
   u32x4 a_reg[C::A_CHUNKS], b_reg[C::B_CHUNKS];
+  // Global -> registers for the stage at k0. Full stages load unconditionally; the last,
+  // partial stage zero-fills the 16-byte chunks beyond d (d % 8 == 0).
   auto load_stage = [&](int k0) {
+    if (k0 + C::BK <= d) {
 #pragma unroll
-    for (int i = 0; i < C::A_CHUNKS; ++i) {
-      if (k0 + a_col[i] < d)
+      for (int i = 0; i < C::A_CHUNKS; ++i)
         a_reg[i] = *reinterpret_cast<const u32x4*>(a_src[i] + k0);
-      else
-        a_reg[i] = u32x4{0u, 0u, 0u, 0u};
-    }
 #pragma unroll
-    for (int i = 0; i < C::B_CHUNKS; ++i) {
-      if (k0 + b_col[i] < d)
+      for (int i = 0; i < C::B_CHUNKS; ++i)
         b_reg[i] = *reinterpret_cast<const u32x4*>(b_src[i] + k0);
-      else
-        b_reg[i] = u32x4{0u, 0u, 0u, 0u};
+    } else {
+#pragma unroll
+      for (int i = 0; i < C::A_CHUNKS; ++i)
+        a_reg[i] = k0 + a_col[i] < d ? *reinterpret_cast<const u32x4*>(a_src[i] + k0)
+                                     : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int i = 0; i < C::B_CHUNKS; ++i)
+        b_reg[i] = k0 + b_col[i] < d ? *reinterpret_cast<const u32x4*>(b_src[i] + k0)
+                                     : u32x4{0u, 0u, 0u, 0u};
     }
   };
   auto store_stage = [&](int buf) {
@@ -143,90 +245,267 @@ __global__ __launch_bounds__(C::kThreads, 2) void head_bf16_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.0f;
 
+  // MFMA operand fragments: lane l reads row l % 32 of a 32-row block and the 8 consecutive
+  // k values starting at 8 (l / 32) of the current 16-wide k step.
+  const int frag_row = lane & 31;
+  const int frag_k = (lane >> 5) * 8;
+  const int a_frag = (wv * kVTile + frag_row) * C::LDK + frag_k;
+  const int b_frag = (wm * C::TM + frag_row) * C::LDK + frag_k;
+  bf16x8 af[2][C::NRB], bfr[2][C::NCB];
+  auto load_frags = [&](int set, int buf, int kk) {
+#pragma unroll
+    for (int rb = 0; rb < C::NRB; ++rb)
+      af[set][rb] = *reinterpret_cast<const bf16x8*>(&As[buf][a_frag + rb * 32 * C::LDK + kk]);
+#pragma unroll
+    for (int cb = 0; cb < C::NCB; ++cb)
+      bfr[set][cb] = *reinterpret_cast<const bf16x8*>(&Bs[buf][b_frag + cb * 32 * C::LDK + kk]);
+  };
+
+  constexpr int KSTEPS = C::BK / 16;
   const int nk = (d + C::BK - 1) / C::BK;
   load_stage(0);
   store_stage(0);
   __syncthreads();
+  load_frags(0, 0, 0);
 
-  const int frag_row = lane & 31;
-  const int frag_k = (lane >> 5) * 8;
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) load_stage((kt + 1) * C::BK);
+    const bool more = kt + 1 < nk;
+    if (more) load_stage((kt + 1) * C::BK);
 #pragma unroll
-    for (int kk = 0; kk < C::BK; kk += 16) {
-      bf16x8 af[C::NRB], bfr[C::NCB];
-#pragma unroll
-      for (int rb = 0; rb < C::NRB; ++rb)
-        af[rb] = *reinterpret_cast<const bf16x8*>(
-            &As[buf][(wv * kVTile + rb * 32 + frag_row) * C::LDK + kk + frag_k]);
-#pragma unroll
-      for (int cb = 0; cb < C::NCB; ++cb)
-        bfr[cb] = *reinterpret_cast<const bf16x8*>(
-            &Bs[buf][(wm * C::TM + cb * 32 + frag_row) * C::LDK + kk + frag_k]);
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      const int cur = ks & 1;
+      // Fetch the next k step's fragments while this step's MFMAs run.
+      if (ks + 1 < KSTEPS) load_frags(cur ^ 1, buf, (ks + 1) * 16);
 #pragma unroll
       for (int rb = 0; rb < C::NRB; ++rb)
 #pragma unroll
         for (int cb = 0; cb < C::NCB; ++cb)
-          acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[rb], bfr[cb], acc[rb][cb],
-                                                                 0, 0, 0);
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][rb], bfr[cur][cb],
+                                                                 acc[rb][cb], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_stage(buf ^ 1);
+    if (more) store_stage(buf ^ 1);
     __syncthreads();
+    if (more) load_frags(0, buf ^ 1, 0);
   }
 
-  // Epilogue: this wave holds the logits of vocabulary tile t for TM branch rows. Lane l holds
-  // column (branch row) l % 32 of each 32-column block and, in register r of row block rb,
-  // vocabulary id v0w + 32 rb + 8 (r / 4) + 4 (l / 32) + r % 4.
   const int64_t v0w = v0 + wv * kVTile;
   if (v0w >= V) return;
-  const int t = static_cast<int>(v0w / kVTile);
-  const int half = lane >> 5;
+  tile_logsoftmax_store<C::NRB, C::NCB>(acc, tls, lmass, M, V, nT, v0w, m0 + wm * C::TM, lane,
+                                        vec4);
+}
+
+// ---------------------------------------------------------------------------------------
+// Direct-to-LDS variant (hidden sizes that are a multiple of BK): operand tiles are copied
+// global -> LDS by global_load_lds_dwordx4 into an S-stage ring, issued S - 1 stages ahead, so
+// no staging registers are needed and global latency is covered by S - 1 stages of MFMA work.
+// LDS rows hold BK bf16; the 16-byte chunks of row r are XOR-permuted by swz(r) so that the
+// MFMA fragment reads are free of bank conflicts: ds_read_b128 serves 16 consecutive lanes per
+// cycle from 64 four-byte banks (256 B), so rows r, r + 4, r + 8, r + 12 of a 64-byte-row tile
+// must land their chunk in different 16-byte bank groups (measured with SQ_LDS_BANK_CONFLICT).
+template <int BK_, int S_>
+struct DmaCfg {
+  static constexpr int BV = 256, BM = 256, BK = BK_, S = S_;
+  static constexpr int kThreads = 256, WM = 2, TM = 128, NCB = 4, NRB = 4;
+  static constexpr int CPR = BK / 8;                     // 16-byte chunks per row
+  static constexpr int ROWB = BK * 2;                    // bytes per LDS row
+  static constexpr int RPI = 64 / CPR;                   // rows per DMA instruction
+  static constexpr int A_INST = BV / RPI / 4;            // DMA instructions per wave, w rows
+  static constexpr int B_INST = BM / RPI / 4;            // DMA instructions per wave, h rows
+  static constexpr int PER_STAGE = A_INST + B_INST;      // DMA instructions per wave per stage
+  static constexpr int TB = BV * ROWB;                   // bytes of one operand tile
+  static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
+  static_assert(S >= 2 && S <= 5, "2 to 5 stages");
+  static_assert((S - 2) * PER_STAGE <= 63, "vmcnt range");
+};
+
+template <int CPR>
+__device__ __forceinline__ int dma_swz(int r) {
+  return CPR == 4 ? ((r >> 2) & 3) : ((r >> 1) & 7);
+}
+
+// One global_load_lds_dwordx4: lane i copies 16 bytes from sbase + voff (its own offset) to
+// LDS byte M0 + 16 i. Issued through inline asm so that the compiler does not model the LDS write: its
+// conservative wait-count insertion would otherwise drain every outstanding stage before each
+// LDS read. Completion is tracked explicitly with wait_vmcnt.
+__device__ __forceinline__ void lds_dma16(const char* sbase, uint32_t voff, uint32_t m0v) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "{m0}"(m0v)
+               : "memory");
+}
+
+// LDS byte address of a __shared__ location (the value M0 expects).
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) char*)(p)));
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+#ifndef DBL_HEAD_BK
+#define DBL_HEAD_BK 32
+#endif
+#ifndef DBL_HEAD_STAGES
+#define DBL_HEAD_STAGES 4
+#endif
+using DCfg = DmaCfg<DBL_HEAD_BK, DBL_HEAD_STAGES>;
+
+template <class C>
+__global__ __launch_bounds__(C::kThreads, 1) void head_bf16_dma_kernel(
+    const __bf16* __restrict__ h, const __bf16* __restrict__ w, float* __restrict__ tls,
+    float* __restrict__ lmass, int64_t M, int64_t V, int d, int nT, int n_mtiles, int vec4) {
+  constexpr int TB = C::TB;
+  __shared__ __attribute__((aligned(1024))) char sA0[TB], sB0[TB], sA1[TB], sB1[TB];
+  __shared__ __attribute__((aligned(1024))) char sA2[C::S > 2 ? TB : 16], sB2[C::S > 2 ? TB : 16];
+  __shared__ __attribute__((aligned(1024))) char sA3[C::S > 3 ? TB : 16], sB3[C::S > 3 ? TB : 16];
+  __shared__ __attribute__((aligned(1024))) char sA4[C::S > 4 ? TB : 16], sB4[C::S > 4 ? TB : 16];
+  char* const sA[5] = {sA0, sA1, sA2, sA3, sA4};
+  char* const sB[5] = {sB0, sB1, sB2, sB3, sB4};
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar address math
+  const int wv = wave / C::WM;
+  const int wm = wave % C::WM;
+
+  int vt, mt;
+  tile_of(xcd_remap(blockIdx.x, gridDim.x), gridDim.x / n_mtiles, n_mtiles, &vt, &mt);
+  const int64_t v0 = static_cast<int64_t>(vt) * C::BV;
+  const int64_t m0 = static_cast<int64_t>(mt) * C::BM;
+
+  // DMA sources: instruction i of this wave covers tile rows (wave * INST + i) * RPI + [0, RPI);
+  // lane -> row lane / CPR of it and the chunk whose permuted slot is lane % CPR. Addresses are
+  // a scalar tile base plus a 32-bit per-lane byte offset (rows past V or M are clamped).
+  const char* a_tile = reinterpret_cast<const char*>(w + v0 * d);
+  const char* b_tile = reinterpret_cast<const char*>(h + m0 * d);
+  uint32_t a_off[C::A_INST], b_off[C::B_INST];
 #pragma unroll
-  for (int cb = 0; cb < C::NCB; ++cb) {
-    const int64_t m = m0 + wm * C::TM + cb * 32 + (lane & 31);
-    float mx = -INFINITY;
+  for (int i = 0; i < C::A_INST; ++i) {
+    const int r = (wave * C::A_INST + i) * C::RPI + lane / C::CPR;
+    const int c = (lane % C::CPR) ^ dma_swz<C::CPR>(r);
+    const int64_t gv = v0 + r < V ? r : V - 1 - v0;
+    a_off[i] = static_cast<uint32_t>(gv * d * 2 + c * 16);
+  }
 #pragma unroll
-    for (int rb = 0; rb < C::NRB; ++rb)
+  for (int i = 0; i < C::B_INST; ++i) {
+    const int r = (wave * C::B_INST + i) * C::RPI + lane / C::CPR;
+    const int c = (lane % C::CPR) ^ dma_swz<C::CPR>(r);
+    const int64_t gm = m0 + r < M ? r : M - 1 - m0;
+    b_off[i] = static_cast<uint32_t>(gm * d * 2 + c * 16);
+  }
+
+  f32x16 acc[C::NRB][C::NCB];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t v = v0w + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (v < V) mx = fmaxf(mx, acc[rb][cb][r]);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    float s = 0.0f;
+  for (int rb = 0; rb < C::NRB; ++rb)
 #pragma unroll
-    for (int rb = 0; rb < C::NRB; ++rb)
+    for (int cb = 0; cb < C::NCB; ++cb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t v = v0w + rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (v < V) s += __expf(acc[rb][cb][r] - mx);
-      }
-    s += __shfl_xor(s, 32);
-    const float lm = mx + __logf(s);
-    if (m < M) {
-      float* row = tls + m * V;
-      if (half == 0) lmass[m * nT + t] = lm;
+      for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.0f;
+
+  // Fragment addressing: row = block base + lane % 32, chunk (2 ks + lane / 32) ^ swz(row);
+  // swz(row) depends on row % 32 = lane % 32 only (block bases are multiples of 32), so the
+  // per-k-step offset is a XOR with 32 ks.
+  const int tt = 16 * ((lane >> 5) ^ dma_swz<C::CPR>(lane & 31));
+  const int a_base = (wv * kVTile + (lane & 31)) * C::ROWB;
+  const int b_base = (wm * C::TM + (lane & 31)) * C::ROWB;
+  bf16x8 af[2][C::NRB], bfr[2][C::NCB];
+  // Fragment i of a k step: i < NRB is A block i, else B block i - NRB.
+  auto load_frag = [&](int set, const char* As, const char* Bs, int ks, int i) {
+    const int x = (32 * ks) ^ tt;
+    if (i < C::NRB)
+      af[set][i] = *reinterpret_cast<const bf16x8*>(As + a_base + i * 32 * C::ROWB + x);
+    else
+      bfr[set][i - C::NRB] =
+          *reinterpret_cast<const bf16x8*>(Bs + b_base + (i - C::NRB) * 32 * C::ROWB + x);
+  };
+  auto mfma = [&](int set, int q) {
+    const int rb = q / C::NCB, cb = q % C::NCB;
+    acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[set][rb], bfr[set][cb], acc[rb][cb],
+                                                           0, 0, 0);
+  };
+  auto issue_one = [&](auto slot_c, int k0, int i) {
+    constexpr int slot = decltype(slot_c)::value;
+    if (i < C::A_INST)
+      lds_dma16(a_tile + 2 * k0, a_off[i], lds_addr(sA[slot]) + (wave * C::A_INST + i) * 1024);
+    else
+      lds_dma16(b_tile + 2 * k0, b_off[i - C::A_INST],
+                lds_addr(sB[slot]) + (wave * C::B_INST + i - C::A_INST) * 1024);
+  };
+  constexpr int NF = C::NRB + C::NCB;         // fragments per k step (8)
+  constexpr int NQ = C::NRB * C::NCB;         // MFMAs per k step (16)
+  static_assert(C::BK == 32 && NF == 8 && NQ == 16 && C::PER_STAGE == 8, "pipeline shape");
+
+  const int nk = d / C::BK;
+  // Prologue: stages 0 .. S-2 in flight, stage 0 visible, its first-k-step fragments loaded.
+  // (Stages past nk - 1 repeat stage nk - 1 into unused slots.)
 #pragma unroll
-      for (int rb = 0; rb < C::NRB; ++rb)
+  for (int j = 0; j < C::S - 1; ++j) {
+    const int kj = min(j, nk - 1) * C::BK;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int64_t v = v0w + rb * 32 + 8 * g + 4 * half;
-          if (vec4 && v + 3 < V) {
-            float4 o;
-            o.x = acc[rb][cb][4 * g + 0] - lm;
-            o.y = acc[rb][cb][4 * g + 1] - lm;
-            o.z = acc[rb][cb][4 * g + 2] - lm;
-            o.w = acc[rb][cb][4 * g + 3] - lm;
-            *reinterpret_cast<float4*>(row + v) = o;
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (v + e < V) row[v + e] = acc[rb][cb][4 * g + e] - lm;
-          }
-        }
+    for (int i = 0; i < C::PER_STAGE; ++i) {
+      if (j == 0) issue_one(std::integral_constant<int, 0>{}, kj, i);
+      if (j == 1) issue_one(std::integral_constant<int, 1>{}, kj, i);
+      if (j == 2) issue_one(std::integral_constant<int, 2 % C::S>{}, kj, i);
+      if (j == 3) issue_one(std::integral_constant<int, 3 % C::S>{}, kj, i);
     }
   }
+  wait_vmcnt<(C::S - 2) * C::PER_STAGE>();
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < NF; ++i) load_frag(0, sA[0], sB[0], 0, i);
+
+  // Iteration kt computes stage kt (slot kt % S). First half: k step 0 with fragment set 0,
+  // interleaved with the loads of k step 1 (set 1) and the DMA of stage kt + S - 1 into the
+  // slot of stage kt - 1. Then wait for stage kt + 1, barrier. Second half: k step 1, with
+  // the loads of stage kt + 1's first fragments (set 0).
+  auto body = [&](auto j_c, int kt) {
+    constexpr int j = decltype(j_c)::value;
+    constexpr int jn = (j + 1) % C::S;            // slot of stage kt + 1
+    constexpr int jd = (j + C::S - 1) % C::S;     // slot receiving stage kt + S - 1
+    // Stage kt + S - 1 goes to the slot of stage kt - 1, which every wave has finished reading.
+    // Past the last stage the copy is repeated from stage nk - 1 into that free slot: the loads
+    // stay unconditional, so the outstanding count per wave is always S - 2 stages.
+    const int kd = min(kt + C::S - 1, nk - 1) * C::BK;
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+      mfma(0, 2 * i);
+      mfma(0, 2 * i + 1);
+      load_frag(1, sA[j], sB[j], 1, i);
+      issue_one(std::integral_constant<int, jd>{}, kd, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const bool next = kt + 1 < nk;
+    if (next) {
+      wait_vmcnt<(C::S - 2) * C::PER_STAGE>();
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+    }
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+      mfma(1, 2 * i);
+      mfma(1, 2 * i + 1);
+      if (next) load_frag(0, sA[jn], sB[jn], 0, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  for (int kt0 = 0; kt0 < nk; kt0 += C::S) {
+    body(std::integral_constant<int, 0>{}, kt0);
+    if (kt0 + 1 < nk) body(std::integral_constant<int, 1>{}, kt0 + 1);
+    if (C::S > 2 && kt0 + 2 < nk) body(std::integral_constant<int, 2 % C::S>{}, kt0 + 2);
+    if (C::S > 3 && kt0 + 3 < nk) body(std::integral_constant<int, 3 % C::S>{}, kt0 + 3);
+    if (C::S > 4 && kt0 + 4 < nk) body(std::integral_constant<int, 4 % C::S>{}, kt0 + 4);
+  }
+
+  wait_vmcnt<0>();
+
+  const int64_t v0w = v0 + wv * kVTile;
+  if (v0w >= V) return;
+  tile_logsoftmax_store<C::NRB, C::NCB>(acc, tls, lmass, M, V, nT, v0w, m0 + wm * C::TM, lane,
+                                        vec4);
 }
 
 // fp32 path: workgroup (vocabulary tile t, 4 branch rows); thread j owns id 128 t + j.
@@ -315,10 +594,20 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
     const int64_t nwg = n_vtiles * n_mtiles;
     if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
     const int vec4 = (a.V % 4 == 0) ? 1 : 0;
-    hipLaunchKernelGGL(head_bf16_kernel<Cfg>, dim3(static_cast<unsigned>(nwg)),
-                       dim3(Cfg::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
-                       static_cast<const __bf16*>(a.w), a.tls, a.lmass, a.M, a.V, a.d, nT,
-                       n_mtiles, vec4);
+    if (a.d % DCfg::BK == 0) {
+      const int dm = static_cast<int>((a.M + DCfg::BM - 1) / DCfg::BM);
+      const int64_t dwg = ((a.V + DCfg::BV - 1) / DCfg::BV) * dm;
+      if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
+      hipLaunchKernelGGL(head_bf16_dma_kernel<DCfg>, dim3(static_cast<unsigned>(dwg)),
+                         dim3(DCfg::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
+                         static_cast<const __bf16*>(a.w), a.tls, a.lmass, a.M, a.V, a.d, nT, dm,
+                         vec4);
+    } else {
+      hipLaunchKernelGGL(head_bf16_kernel<Cfg>, dim3(static_cast<unsigned>(nwg)),
+                         dim3(Cfg::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
+                         static_cast<const __bf16*>(a.w), a.tls, a.lmass, a.M, a.V, a.d, nT,
+                         n_mtiles, vec4);
+    }
   } else {
     const int64_t mblocks = (a.M + kF32Rows - 1) / kF32Rows;
     if (mblocks > 65535) return hipErrorInvalidConfiguration;
