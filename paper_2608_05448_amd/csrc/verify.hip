@@ -71,41 +71,167 @@ __global__ __launch_bounds__(64) void chain_kernel(VerifyArgs a) {
   }
 }
 
-// Acceptance-mass stream. Thread i of the workgroup handles 4 consecutive ids per step.
+// Parallel form of chain_kernel for K * R <= kChainMaxKR and K <= kChainMaxK (one workgroup
+// per block). The posterior at position k depends only on the drafted prefix, not on the
+// accept decisions, so every position is handled at once: thread (k, z) folds its own prefix
+// L_{k,z} = (((L_{0,z} + lq_{0,z}) + lq_{1,z}) + ...) + lq_{k-1,z} in the same order as the
+// sequential walk, wavefront k normalises it and forms q_k(x_k | x_<k), and one thread then
+// runs the integer accept chain over k. Bit-identical to chain_kernel.
+constexpr int kChainMaxKR = 2048;
+constexpr int kChainMaxK = 256;
+
+__global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
+  const BlockArgs& k_ = a.blk;
+  const int64_t b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid >> 6;
+  const int R = static_cast<int>(k_.R);
+  const int K = static_cast<int>(k_.K);
+  const int KR = K * R;
+  const uint64_t seq = static_cast<uint64_t>(k_.seq_offset + b);
+  __shared__ float s_lq[kChainMaxKR];
+  __shared__ double s_L[kChainMaxKR];
+  __shared__ double s_L0[kMaxR];
+  __shared__ double s_Q[kChainMaxK];
+  __shared__ double s_P[kChainMaxK];
+  if (wave == 0) {
+    const double l0 = prior_log_weight(k_.prior + b * k_.R, R, k_.z_temp);
+    if (lane < R) s_L0[lane] = l0;
+  }
+  for (int i = tid; i < KR; i += blockDim.x) {
+    const int k = i / R, z = i % R;
+    const int64_t row = (b * k_.K + k) * k_.R + z;
+    const int32_t xk = a.x[b * k_.K + k];
+    s_lq[i] = in_vocab(xk, k_.V)
+                  ? flat_lq(k_.tls[row * k_.V + xk], k_.lmass[row * k_.nT + xk / kTile], k_.lse[row])
+                  : -INFINITY;
+  }
+  if (!a.trajectory) {
+    for (int k = tid; k < K; k += blockDim.x) {
+      const int32_t xk = a.x[b * k_.K + k];
+      s_P[k] = in_vocab(xk, k_.V)
+                   ? static_cast<double>(detexp32(a.logp[(b * a.Kp + k) * k_.V + xk]))
+                   : 0.0;
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < KR; i += blockDim.x) {
+    const int k = i / R, z = i % R;
+    double L = s_L0[z];
+    for (int j = 0; j < k; ++j) L = __dadd_rn(L, static_cast<double>(s_lq[j * R + z]));
+    s_L[i] = L;
+  }
+  __syncthreads();
+  const int nwaves = blockDim.x >> 6;
+  for (int k = wave; k < K; k += nwaves) {
+    const double L = lane < R ? s_L[k * R + lane] : -INFINITY;
+    const double w = normalize_weight(L, R);
+    if (lane < R) a.wpost[(b * k_.K + k) * k_.R + lane] = w;
+    if (!a.trajectory) {
+      const double y = lane < R ? static_cast<double>(detexp32(s_lq[k * R + lane])) : 0.0;
+      double Q = 0.0;
+      for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, __dmul_rn(__shfl(w, z), __shfl(y, z)));
+      if (lane == 0) s_Q[k] = Q;
+    }
+  }
+  if (a.trajectory) return;
+  __syncthreads();
+  if (tid == 0) {
+    bool alive = true;
+    int n_acc = 0;
+    double prodA = 1.0, al = 0.0;
+    for (int k = 0; k < K; ++k) {
+      const double Q = s_Q[k], P = s_P[k];
+      const double A = Q > 0.0 ? fmin(1.0, P / Q) : (P > 0.0 ? 1.0 : 0.0);
+      prodA = __dmul_rn(prodA, A);
+      al = __dadd_rn(al, prodA);
+      if (alive) {
+        const uint32_t r = draw(k_.seed, kAccept, static_cast<uint32_t>(k), seq, k_.step);
+        if (accept_int(r, quant40d(Q), quant40d(P)))
+          ++n_acc;
+        else
+          alive = false;
+      }
+    }
+    a.n_accept[b] = n_acc;
+    if (a.al) a.al[b] = static_cast<float>(al);
+  }
+}
+
+// Acceptance-mass stream: workgroup (position, chunk of kTilesPerChunk vocabulary tiles).
+// beta partial = sum_v min(p(v), sum_z w_z q_z(v)) over the chunk, with p = exp(logp) and
+// q_z = exp(tls + lmass - lse) evaluated as exp2(tls * log2 e + o_z,t), the per-tile offsets
+// o_z,t prepared once in LDS. Every row is streamed once with 16-byte loads; RT > 0 fixes the
+// number of categories at compile time so all R + 1 loads of a step are in flight together.
+constexpr float kLog2eF = 1.4426950408889634f;
+
+template <int RT>
 __global__ __launch_bounds__(256) void beta_kernel(VerifyArgs a) {
   const BlockArgs& k_ = a.blk;
   const int64_t pos = blockIdx.x;
   const int64_t b = pos / k_.K;
   const int64_t k = pos % k_.K;
-  const int R = static_cast<int>(k_.R);
-  __shared__ float wz[kMaxR];
+  const int R = RT > 0 ? RT : static_cast<int>(k_.R);
+  const int64_t V = k_.V;
+  __shared__ float s_w[kMaxR];
+  __shared__ float s_off[kMaxR][kTilesPerChunk];
   __shared__ float red[4];
-  if (threadIdx.x < R) wz[threadIdx.x] = static_cast<float>(a.wpost[pos * k_.R + threadIdx.x]);
-  __syncthreads();
-  const int64_t v_begin = static_cast<int64_t>(blockIdx.y) * kTilesPerChunk * kTile;
-  const int64_t v_end = min(k_.V, v_begin + static_cast<int64_t>(kTilesPerChunk) * kTile);
-  const float* prow = a.logp + (b * a.Kp + k) * k_.V;
+  const int t0 = blockIdx.y * kTilesPerChunk;
+  const int nt = min(kTilesPerChunk, k_.nT - t0);
   const int64_t m0 = pos * k_.R;
+  for (int i = threadIdx.x; i < R * kTilesPerChunk; i += blockDim.x) {
+    const int z = i / kTilesPerChunk, tt = i % kTilesPerChunk;
+    if (tt < nt)
+      s_off[z][tt] = (k_.lmass[(m0 + z) * k_.nT + t0 + tt] - k_.lse[m0 + z]) * kLog2eF;
+  }
+  if (threadIdx.x < R) s_w[threadIdx.x] = static_cast<float>(a.wpost[m0 + threadIdx.x]);
+  __syncthreads();
+  const int64_t vb = static_cast<int64_t>(t0) * kTile;
+  const int64_t ve = min(V, vb + static_cast<int64_t>(nt) * kTile);
+  const float* prow = a.logp + (b * a.Kp + k) * V;
+  const float* trow = k_.tls + m0 * V;
   float acc = 0.0f;
-  for (int64_t v = v_begin + 4 * threadIdx.x; v < v_end; v += 4 * blockDim.x) {
-    const int n = static_cast<int>(min<int64_t>(4, v_end - v));
-    float p[4], q[4];
+  if ((V & 3) == 0) {
+    for (int64_t v = vb + 4 * threadIdx.x; v < ve; v += 4 * blockDim.x) {
+      const int tt = static_cast<int>((v - vb) >> 7);
+      const float4 p = *reinterpret_cast<const float4*>(prow + v);
+      float4 x[RT > 0 ? RT : 1];
+      float q0 = 0.0f, q1 = 0.0f, q2 = 0.0f, q3 = 0.0f;
+      if constexpr (RT > 0) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      p[e] = e < n ? __expf(prow[v + e]) : 0.0f;
-      q[e] = 0.0f;
+        for (int z = 0; z < RT; ++z) x[z] = *reinterpret_cast<const float4*>(trow + z * V + v);
+#pragma unroll
+        for (int z = 0; z < RT; ++z) {
+          const float o = s_off[z][tt], w = s_w[z];
+          q0 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(x[z].x, kLog2eF, o)), q0);
+          q1 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(x[z].y, kLog2eF, o)), q1);
+          q2 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(x[z].z, kLog2eF, o)), q2);
+          q3 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(x[z].w, kLog2eF, o)), q3);
+        }
+      } else {
+        for (int z = 0; z < R; ++z) {
+          const float4 xz = *reinterpret_cast<const float4*>(trow + z * V + v);
+          const float o = s_off[z][tt], w = s_w[z];
+          q0 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.x, kLog2eF, o)), q0);
+          q1 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.y, kLog2eF, o)), q1);
+          q2 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.z, kLog2eF, o)), q2);
+          q3 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.w, kLog2eF, o)), q3);
+        }
+      }
+      acc += fminf(__builtin_amdgcn_exp2f(p.x * kLog2eF), q0) +
+             fminf(__builtin_amdgcn_exp2f(p.y * kLog2eF), q1) +
+             fminf(__builtin_amdgcn_exp2f(p.z * kLog2eF), q2) +
+             fminf(__builtin_amdgcn_exp2f(p.w * kLog2eF), q3);
     }
-    const int t = static_cast<int>(v / kTile);
-    for (int z = 0; z < R; ++z) {
-      const int64_t m = m0 + z;
-      const float off = k_.lmass[m * k_.nT + t] - k_.lse[m];
-      const float* row = k_.tls + m * k_.V;
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (e < n) q[e] += wz[z] * __expf(row[v + e] + off);
+  } else {
+    for (int64_t v = vb + threadIdx.x; v < ve; v += blockDim.x) {
+      const int tt = static_cast<int>((v - vb) >> 7);
+      float q = 0.0f;
+      for (int z = 0; z < R; ++z)
+        q = fmaf(s_w[z], __builtin_amdgcn_exp2f(fmaf(trow[z * V + v], kLog2eF, s_off[z][tt])), q);
+      acc += fminf(__builtin_amdgcn_exp2f(prow[v] * kLog2eF), q);
     }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) acc += fminf(p[e], q[e]);
   }
   acc = wave_sum_f32(acc);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
@@ -227,13 +353,24 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
   const int64_t npos = B * a.blk.K;
   const int nchunk = n_chunks(a.blk.nT);
   if (npos > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(chain_kernel, dim3(static_cast<unsigned>(B)), dim3(64), 0, stream, a);
+  if (a.blk.K * a.blk.R <= kChainMaxKR && a.blk.K <= kChainMaxK)
+    hipLaunchKernelGGL(chain_parallel_kernel, dim3(static_cast<unsigned>(B)), dim3(256), 0, stream,
+                       a);
+  else
+    hipLaunchKernelGGL(chain_kernel, dim3(static_cast<unsigned>(B)), dim3(64), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const bool want_beta = a.beta || a.exp_len;
   if (want_beta) {
-    hipLaunchKernelGGL(beta_kernel, dim3(static_cast<unsigned>(npos), nchunk), dim3(256), 0,
-                       stream, a);
+    const dim3 grid(static_cast<unsigned>(npos), nchunk);
+    switch (a.blk.R) {
+      case 1: hipLaunchKernelGGL(beta_kernel<1>, grid, dim3(256), 0, stream, a); break;
+      case 2: hipLaunchKernelGGL(beta_kernel<2>, grid, dim3(256), 0, stream, a); break;
+      case 4: hipLaunchKernelGGL(beta_kernel<4>, grid, dim3(256), 0, stream, a); break;
+      case 8: hipLaunchKernelGGL(beta_kernel<8>, grid, dim3(256), 0, stream, a); break;
+      case 16: hipLaunchKernelGGL(beta_kernel<16>, grid, dim3(256), 0, stream, a); break;
+      default: hipLaunchKernelGGL(beta_kernel<0>, grid, dim3(256), 0, stream, a); break;
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (!a.trajectory) {

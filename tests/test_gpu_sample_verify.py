@@ -28,6 +28,8 @@ CASES = [
     ("greedy-target", 4, 5, 3, 900, 16, "aligned", 1, 0.0, 1.0, 6, 0, 0),
     ("many-blocks", 64, 4, 2, 1000, 16, "aligned", 1, 1.0, 1.0, 7, 11, 123456),
     ("ragged-vocab", 3, 4, 3, 1001, 16, "aligned", 1, 0.6, 1.0, 8, 0, 0),
+    ("long-block", 2, 40, 64, 300, 8, "aligned", 1, 1.0, 1.0, 9, 0, 0),   # K*R > 2048
+    ("wide-categories", 3, 6, 5, 2000, 16, "aligned", 1, 1.0, 2.0, 10, 5, 3),  # R not 1,2,4,8,16
 ]
 
 
