@@ -86,6 +86,44 @@ def _cpu_baseline(wl, h, w, ell, logp, budget_s: float):
                       f"and verification, {el:.1f} s on the host"}
 
 
+def _pmc_mean(csv_dir: str, counter: str, name_re: str) -> float:
+    """Mean over dispatches (of kernels matching name_re) of a counter summed over instances."""
+    import csv
+    import glob
+    import re
+    per = {}
+    for path in glob.glob(os.path.join(csv_dir, "*counter_collection.csv")):
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if row["Counter_Name"] == counter and re.search(name_re, row["Kernel_Name"]):
+                    per[row["Dispatch_Id"]] = per.get(row["Dispatch_Id"], 0.0) + float(
+                        row["Counter_Value"])
+    if not per:
+        raise SystemExit(f"no {counter} rows for /{name_re}/ under {csv_dir}")
+    return sum(per.values()) / len(per)
+
+
+def _write_traffic(head_fetch, head_write, copy_fetch, copy_write, copy_bytes, workload):
+    """HBM bytes per head launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs (KiB per dispatch),
+    each scaled so that the same counter reads exactly copy_bytes for a plain device copy."""
+    hf = _pmc_mean(head_fetch, "FETCH_SIZE", "head_bf16")
+    hw = _pmc_mean(head_write, "WRITE_SIZE", "head_bf16")
+    cf = _pmc_mean(copy_fetch, "FETCH_SIZE", "copyBuffer")
+    cw = _pmc_mean(copy_write, "WRITE_SIZE", "copyBuffer")
+    f_fetch = copy_bytes / (cf * 1024.0)
+    f_write = copy_bytes / (cw * 1024.0)
+    rec = {"workload": workload, "head_source_sha256_16": _head_source_hash(),
+           "fetch_kib_per_launch": hf, "write_kib_per_launch": hw,
+           "copy_bytes": copy_bytes, "copy_fetch_kib": cf, "copy_write_kib": cw,
+           "fetch_scale": f_fetch, "write_scale": f_write,
+           "hbm_read_bytes_per_launch": hf * 1024.0 * f_fetch,
+           "hbm_write_bytes_per_launch": hw * 1024.0 * f_write,
+           "hbm_bytes_per_launch": hf * 1024.0 * f_fetch + hw * 1024.0 * f_write}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
 def _copy_calibration(nbytes: int):
     """A plain device copy of known size, for scaling the FETCH_SIZE / WRITE_SIZE counters."""
     import torch
@@ -108,7 +146,17 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", type=int, default=0)
+    ap.add_argument("--write-traffic", nargs=5, metavar=("HEAD_FETCH_DIR", "HEAD_WRITE_DIR",
+                                                         "COPY_FETCH_DIR", "COPY_WRITE_DIR",
+                                                         "COPY_BYTES"),
+                    help="turn rocprofv3 FETCH_SIZE/WRITE_SIZE CSV output into the committed "
+                         "per-launch traffic record (no GPU work)")
     args = ap.parse_args(argv)
+
+    if args.write_traffic:
+        hf, hw, cf, cw, nb = args.write_traffic
+        _write_traffic(hf, hw, cf, cw, int(nb), args.workload)
+        return 0
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the hot "
