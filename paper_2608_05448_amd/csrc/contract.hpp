@@ -103,9 +103,16 @@ __device__ __forceinline__ double dexp64(double x) {
 // ---------------------------------------------------------------------------------------
 // Fixed point and integer decisions
 // ---------------------------------------------------------------------------------------
-// floor(y * 2^40) for y in [0, 1] (exact: scaling by a power of two, then truncation).
+// floor(y * 2^40) for binary32 y in [0, 1], exactly, from the bits of y: a normal y equals
+// mant * 2^(e - 150), so y * 2^40 = mant * 2^(e - 110) and the floor is a shift of the 24-bit
+// significand. Zero and subnormals (< 2^-126) give 0.
 __device__ __forceinline__ uint64_t quant40(float y) {
-  return static_cast<uint64_t>(static_cast<double>(y) * 0x1p40);
+  const uint32_t u = __float_as_uint(y);
+  const int e = static_cast<int>((u >> 23) & 0xffu);
+  if (e == 0) return 0;
+  const uint64_t m = static_cast<uint64_t>((u & 0x7fffffu) | 0x800000u);
+  const int sh = e - 110;
+  return sh >= 0 ? (m << sh) : (sh > -24 ? (m >> -sh) : 0);
 }
 __device__ __forceinline__ uint64_t quant40d(double y) {
   return static_cast<uint64_t>(y * 0x1p40);

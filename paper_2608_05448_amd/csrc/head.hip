@@ -303,20 +303,24 @@ __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_kernel(
 // MFMA fragment reads are free of bank conflicts: ds_read_b128 serves 16 consecutive lanes per
 // cycle from 64 four-byte banks (256 B), so rows r, r + 4, r + 8, r + 12 of a 64-byte-row tile
 // must land their chunk in different 16-byte bank groups (measured with SQ_LDS_BANK_CONFLICT).
-template <int BK_, int S_>
+template <int BK_, int S_, int BM_>
 struct DmaCfg {
-  static constexpr int BV = 256, BM = 256, BK = BK_, S = S_;
-  static constexpr int kThreads = 256, WM = 2, TM = 128, NCB = 4, NRB = 4;
+  static constexpr int BV = 256, BM = BM_, BK = BK_, S = S_;
+  static constexpr int kThreads = 256, WM = 2, TM = BM / 2, NCB = TM / 32, NRB = 4;
+  static constexpr int kWgPerCu = BM == 256 ? 1 : 2;     // co-resident workgroups per CU
   static constexpr int CPR = BK / 8;                     // 16-byte chunks per row
   static constexpr int ROWB = BK * 2;                    // bytes per LDS row
   static constexpr int RPI = 64 / CPR;                   // rows per DMA instruction
   static constexpr int A_INST = BV / RPI / 4;            // DMA instructions per wave, w rows
   static constexpr int B_INST = BM / RPI / 4;            // DMA instructions per wave, h rows
   static constexpr int PER_STAGE = A_INST + B_INST;      // DMA instructions per wave per stage
-  static constexpr int TB = BV * ROWB;                   // bytes of one operand tile
+  static constexpr int TBA = BV * ROWB;                  // bytes of the w tile of one stage
+  static constexpr int TBB = BM * ROWB;                  // bytes of the h tile of one stage
   static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
+  static_assert(BM == 128 || BM == 256, "branch-row tile of 128 or 256");
   static_assert(S >= 2 && S <= 5, "2 to 5 stages");
   static_assert((S - 2) * PER_STAGE <= 63, "vmcnt range");
+  static_assert(S * (TBA + TBB) * kWgPerCu <= 160 * 1024, "LDS per CU");
 };
 
 template <int CPR>
@@ -350,17 +354,20 @@ __device__ __forceinline__ void wait_vmcnt() {
 #ifndef DBL_HEAD_STAGES
 #define DBL_HEAD_STAGES 4
 #endif
-using DCfg = DmaCfg<DBL_HEAD_BK, DBL_HEAD_STAGES>;
+#ifndef DBL_HEAD_BM
+#define DBL_HEAD_BM 256
+#endif
+using DCfg = DmaCfg<DBL_HEAD_BK, DBL_HEAD_STAGES, DBL_HEAD_BM>;
 
 template <class C>
-__global__ __launch_bounds__(C::kThreads, 1) void head_bf16_dma_kernel(
+__global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel(
     const __bf16* __restrict__ h, const __bf16* __restrict__ w, float* __restrict__ tls,
     float* __restrict__ lmass, int64_t M, int64_t V, int d, int nT, int n_mtiles, int vec4) {
-  constexpr int TB = C::TB;
-  __shared__ __attribute__((aligned(1024))) char sA0[TB], sB0[TB], sA1[TB], sB1[TB];
-  __shared__ __attribute__((aligned(1024))) char sA2[C::S > 2 ? TB : 16], sB2[C::S > 2 ? TB : 16];
-  __shared__ __attribute__((aligned(1024))) char sA3[C::S > 3 ? TB : 16], sB3[C::S > 3 ? TB : 16];
-  __shared__ __attribute__((aligned(1024))) char sA4[C::S > 4 ? TB : 16], sB4[C::S > 4 ? TB : 16];
+  constexpr int TA = C::TBA, TB = C::TBB;
+  __shared__ __attribute__((aligned(1024))) char sA0[TA], sB0[TB], sA1[TA], sB1[TB];
+  __shared__ __attribute__((aligned(1024))) char sA2[C::S > 2 ? TA : 16], sB2[C::S > 2 ? TB : 16];
+  __shared__ __attribute__((aligned(1024))) char sA3[C::S > 3 ? TA : 16], sB3[C::S > 3 ? TB : 16];
+  __shared__ __attribute__((aligned(1024))) char sA4[C::S > 4 ? TA : 16], sB4[C::S > 4 ? TB : 16];
   char* const sA[5] = {sA0, sA1, sA2, sA3, sA4};
   char* const sB[5] = {sB0, sB1, sB2, sB3, sB4};
 
@@ -433,9 +440,12 @@ __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_dma_kernel(
       lds_dma16(b_tile + 2 * k0, b_off[i - C::A_INST],
                 lds_addr(sB[slot]) + (wave * C::B_INST + i - C::A_INST) * 1024);
   };
-  constexpr int NF = C::NRB + C::NCB;         // fragments per k step (8)
-  constexpr int NQ = C::NRB * C::NCB;         // MFMAs per k step (16)
-  static_assert(C::BK == 32 && NF == 8 && NQ == 16 && C::PER_STAGE == 8, "pipeline shape");
+  constexpr int NF = C::NRB + C::NCB;         // fragments per k step
+  constexpr int NQ = C::NRB * C::NCB;         // MFMAs per k step
+  constexpr int NSLOT = NQ / 2;               // MFMA pairs per k step
+  static_assert(C::BK == 32, "the pipeline interleaves two 16-deep k steps per stage");
+  // Slot i of a k step issues MFMA pair i, then fragments [i NF / NSLOT, (i + 1) NF / NSLOT)
+  // and DMA instructions [i P / NSLOT, (i + 1) P / NSLOT).
 
   const int nk = d / C::BK;
   // Prologue: stages 0 .. S-2 in flight, stage 0 visible, its first-k-step fragments loaded.
@@ -470,11 +480,14 @@ __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_dma_kernel(
     // stay unconditional, so the outstanding count per wave is always S - 2 stages.
     const int kd = min(kt + C::S - 1, nk - 1) * C::BK;
 #pragma unroll
-    for (int i = 0; i < NF; ++i) {
+    for (int i = 0; i < NSLOT; ++i) {
       mfma(0, 2 * i);
       mfma(0, 2 * i + 1);
-      load_frag(1, sA[j], sB[j], 1, i);
-      issue_one(std::integral_constant<int, jd>{}, kd, i);
+#pragma unroll
+      for (int f = i * NF / NSLOT; f < (i + 1) * NF / NSLOT; ++f) load_frag(1, sA[j], sB[j], 1, f);
+#pragma unroll
+      for (int q = i * C::PER_STAGE / NSLOT; q < (i + 1) * C::PER_STAGE / NSLOT; ++q)
+        issue_one(std::integral_constant<int, jd>{}, kd, q);
       __builtin_amdgcn_sched_barrier(0);
     }
     const bool next = kt + 1 < nk;
@@ -485,10 +498,14 @@ __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_dma_kernel(
       asm volatile("" ::: "memory");
     }
 #pragma unroll
-    for (int i = 0; i < NF; ++i) {
+    for (int i = 0; i < NSLOT; ++i) {
       mfma(1, 2 * i);
       mfma(1, 2 * i + 1);
-      if (next) load_frag(0, sA[jn], sB[jn], 0, i);
+      if (next) {
+#pragma unroll
+        for (int f = i * NF / NSLOT; f < (i + 1) * NF / NSLOT; ++f)
+          load_frag(0, sA[jn], sB[jn], 0, f);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -575,13 +592,22 @@ __global__ __launch_bounds__(256) void lse_finalize_kernel(const float* __restri
   const int lane = threadIdx.x & 63;
   if (m >= M) return;
   const float* row = lmass + m * nT;
-  float mx = -INFINITY;
-  for (int t = lane; t < nT; t += 64) mx = fmaxf(mx, row[t]);
-  mx = wave_max(mx);
-  float s = 0.0f;
-  for (int t = lane; t < nT; t += 64) s += __expf(row[t] - mx);
+  // Single pass: every lane keeps a running (max, sum of exp relative to max) pair, and the
+  // pairs are merged across the wavefront.
+  float mx = -INFINITY, s = 0.0f;
+  for (int t = lane; t < nT; t += 64) {
+    const float x = row[t];
+    if (x > mx) {
+      s = s * __expf(mx - x) + 1.0f;
+      mx = x;
+    } else if (x > -INFINITY) {
+      s += __expf(x - mx);
+    }
+  }
+  const float gmx = wave_max(mx);
+  s = mx > -INFINITY ? s * __expf(mx - gmx) : 0.0f;
   s = wave_sum(s);
-  if (lane == 0) lse[m] = mx + __logf(s);
+  if (lane == 0) lse[m] = gmx + __logf(s);
 }
 
 }  // namespace

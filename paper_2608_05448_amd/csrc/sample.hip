@@ -1,11 +1,12 @@
 // Block draw from the DBLast latent mixture (Sec. "Dependent Block Drafting and Verification":
 // draw a category from the prior, then every position of the block in parallel from that
 // branch). Two kernels:
-//   sample_tiles   grid (position, vocabulary chunk): the drawn category's row is streamed
-//                  once; each 128-id tile's integer mass sum_v floor(q(v) 2^40) goes to the
-//                  workspace;
-//   sample_select  one wavefront per position: inverse CDF over the tile sums, then a scan of
-//                  the selected tile.
+//   sample_tiles   grid (position, chunk of 32 vocabulary tiles), 256 threads: the drawn
+//                  category's row is streamed once; 8 lanes per 128-id tile each quantise 16 ids
+//                  (four 16-byte loads) and the tile's exact integer mass
+//                  sum_v floor(q(v) 2^40) goes to the workspace;
+//   sample_select  one 256-thread workgroup per position: inverse CDF over the tile sums, then a
+//                  scan of the selected tile.
 // Built with floating-point contraction off: every probability that decides a draw follows
 // the determinism contract exactly.
 #include <hip/hip_runtime.h>
@@ -23,32 +24,42 @@ __global__ __launch_bounds__(256) void sample_tiles_kernel(SampleArgs a) {
   const int64_t pos = blockIdx.x;
   const int64_t b = pos / k_.K;
   const int64_t k = pos % k_.K;
-  const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
   const int z = draw_category(k_, b);
   if (blockIdx.y == 0 && k == 0 && threadIdx.x == 0) a.z_out[b] = z;
-  uint64_t* out = a.tilesum + pos * k_.nT;
-  const int t_begin = blockIdx.y * kTilesPerChunk;
-  const int t_end = min(k_.nT, t_begin + kTilesPerChunk);
-  if (z < 0) {
-    for (int t = t_begin + static_cast<int>(threadIdx.x); t < t_end; t += blockDim.x) out[t] = 0;
-    return;
+  const int sub = threadIdx.x & 7;                     // lane within the tile's group of 8
+  const int t = blockIdx.y * kTilesPerChunk + (threadIdx.x >> 3);
+  uint64_t s = 0;
+  if (z >= 0 && t < k_.nT) {
+    const int64_t m = (b * k_.K + k) * k_.R + z;
+    const float off = __fsub_rn(k_.lmass[m * k_.nT + t], k_.lse[m]);
+    const int64_t v0 = static_cast<int64_t>(t) * kTile;
+    const float* row = k_.tls + m * k_.V + v0;
+    if ((k_.V & 3) == 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int v = 4 * sub + 32 * i;
+        if (v0 + v < k_.V) {
+          const float4 x = *reinterpret_cast<const float4*>(row + v);
+          s += quant40(detexp32(__fadd_rn(x.x, off))) + quant40(detexp32(__fadd_rn(x.y, off))) +
+               quant40(detexp32(__fadd_rn(x.z, off))) + quant40(detexp32(__fadd_rn(x.w, off)));
+        }
+      }
+    } else {
+#pragma unroll 4
+      for (int i = 0; i < 16; ++i) {
+        const int v = sub + 8 * i;
+        if (v0 + v < k_.V) s += quant40(detexp32(__fadd_rn(row[v], off)));
+      }
+    }
   }
-  const int64_t m = (b * k_.K + k) * k_.R + z;
-  const float* row = k_.tls + m * k_.V;
-  const float lse = k_.lse[m];
-  for (int t = t_begin + wave; t < t_end; t += 4) {
-    const float off = __fsub_rn(k_.lmass[m * k_.nT + t], lse);
-    const int64_t v = static_cast<int64_t>(t) * kTile + 2 * lane;
-    uint64_t s = 0;
-    if (v < k_.V) s += quant40(detexp32(__fadd_rn(row[v], off)));
-    if (v + 1 < k_.V) s += quant40(detexp32(__fadd_rn(row[v + 1], off)));
-    s = wave_sum_u64(s);
-    if (lane == 0) out[t] = s;
-  }
+  s += __shfl_xor(s, 1);
+  s += __shfl_xor(s, 2);
+  s += __shfl_xor(s, 4);
+  if (sub == 0 && t < k_.nT) a.tilesum[pos * k_.nT + t] = s;
 }
 
-__global__ __launch_bounds__(64) void sample_select_kernel(SampleArgs a) {
+__global__ __launch_bounds__(256) void sample_select_kernel(SampleArgs a) {
+  __shared__ uint64_t lds[8];
   const BlockArgs& k_ = a.blk;
   const int64_t pos = blockIdx.x;
   const int64_t b = pos / k_.K;
@@ -62,10 +73,10 @@ __global__ __launch_bounds__(64) void sample_select_kernel(SampleArgs a) {
     const float lse = k_.lse[m];
     const uint32_t r = draw(k_.seed, kToken, static_cast<uint32_t>(k),
                             static_cast<uint64_t>(k_.seq_offset + b), k_.step);
-    x = select_by_tiles(a.tilesum + pos * k_.nT, k_.nT, k_.V, r, [&](int64_t v) {
-      const float off = __fsub_rn(lm[v / kTile], lse);
-      return quant40(detexp32(__fadd_rn(row[v], off)));
-    });
+    x = select_by_tiles_block(
+        a.tilesum + pos * k_.nT, k_.nT, k_.V, r,
+        [&](int64_t v) { return quant40(detexp32(__fadd_rn(row[v], __fsub_rn(lm[v / kTile], lse)))); },
+        lds);
   }
   if (threadIdx.x == 0) a.x_out[b * k_.K + k] = x;
 }
@@ -80,7 +91,7 @@ hipError_t launch_sample(const SampleArgs& a, hipStream_t stream) {
                      0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sample_select_kernel, dim3(static_cast<unsigned>(npos)), dim3(64), 0,
+  hipLaunchKernelGGL(sample_select_kernel, dim3(static_cast<unsigned>(npos)), dim3(256), 0,
                      stream, a);
   return hipGetLastError();
 }

@@ -13,8 +13,8 @@
 //   residual  grid (block, vocabulary chunk): integer tile sums of the residual
 //             max(P - Q, 0) at the first rejected position (and of P for the fallback), or of
 //             the bonus row when every position was accepted.
-//   finalize  one wavefront per block: acceptance masses, E = sum_i prod_{j<=i} beta_j, and the
-//             residual/bonus inverse-CDF draw.
+//   finalize  one 256-thread workgroup per block: acceptance masses,
+//             E = sum_i prod_{j<=i} beta_j, and the residual/bonus inverse-CDF draw.
 // The same kernels serve the expected-length reduction along a given trajectory (no accept
 // test, no residual). Built with floating-point contraction off (determinism contract).
 #include <hip/hip_runtime.h>
@@ -266,70 +266,173 @@ struct ResidualWeight {
   }
 };
 
+// Residual / bonus tile sums: workgroup (block, chunk of 32 vocabulary tiles), 8 lanes per
+// tile, each lane 16 ids read with 16-byte loads. At the first rejected position ks the integer
+// weights are P(v) = floor(detexp32(logp) 2^40) and R(v) = max(P(v) - Q(v), 0) with
+// Q(v) = floor((sum over ascending z of w_z detexp32(lq_z(v))) 2^40); after full acceptance
+// only P of the bonus row. RT > 0 fixes the number of categories at compile time.
+template <int RT>
 __global__ __launch_bounds__(256) void residual_kernel(VerifyArgs a) {
   const BlockArgs& k_ = a.blk;
   const int64_t b = blockIdx.x;
-  const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
   const int ks = a.n_accept[b];
   const bool residual = ks < k_.K;
   if (!residual && a.Kp != k_.K + 1) return;
+  const int R = RT > 0 ? RT : static_cast<int>(k_.R);
   __shared__ double wz[kMaxR];
-  if (residual && threadIdx.x < k_.R)
-    wz[threadIdx.x] = a.wpost[(b * k_.K + ks) * k_.R + threadIdx.x];
+  if (residual && threadIdx.x < R) wz[threadIdx.x] = a.wpost[(b * k_.K + ks) * k_.R + threadIdx.x];
   __syncthreads();
-  ResidualWeight W{k_.tls, k_.lmass, k_.lse, a.logp + (b * a.Kp + ks) * k_.V,
-                   (b * k_.K + (residual ? ks : 0)) * k_.R, k_.V, k_.nT,
-                   static_cast<int>(k_.R), wz};
-  const int t_begin = blockIdx.y * kTilesPerChunk;
-  const int t_end = min(k_.nT, t_begin + kTilesPerChunk);
-  for (int t = t_begin + wave; t < t_end; t += 4) {
-    uint64_t sp = 0, sr = 0;
+  const int sub = threadIdx.x & 7;
+  const int t = blockIdx.y * kTilesPerChunk + (threadIdx.x >> 3);
+  const int64_t V = k_.V;
+  uint64_t sp = 0, sr = 0;
+  if (t < k_.nT) {
+    const int64_t v0 = static_cast<int64_t>(t) * kTile;
+    const float* prow = a.logp + (b * a.Kp + ks) * V + v0;
+    const int64_t m0 = (b * k_.K + (residual ? ks : 0)) * k_.R;
+    float off[RT > 0 ? RT : 1];
+    if constexpr (RT > 0) {
+      if (residual) {
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int64_t v = static_cast<int64_t>(t) * kTile + 2 * lane + e;
-      if (v < k_.V) {
-        const uint64_t P = W.p_int(v);
-        sp += P;
-        if (residual) {
-          const uint64_t Q = W.q_int(v);
-          sr += P > Q ? P - Q : 0;
+        for (int z = 0; z < RT; ++z)
+          off[z] = __fsub_rn(k_.lmass[(m0 + z) * k_.nT + t], k_.lse[m0 + z]);
+      }
+    }
+    auto weights = [&](int v, float pv, const float* tv, int tstride, uint64_t& P, uint64_t& Rw) {
+      P = quant40(detexp32(pv));
+      Rw = 0;
+      if (!residual) return;
+      double Q = 0.0;
+      if constexpr (RT > 0) {
+#pragma unroll
+        for (int z = 0; z < RT; ++z)
+          Q = __dadd_rn(Q, __dmul_rn(wz[z], static_cast<double>(
+                                                detexp32(__fadd_rn(tv[z * tstride], off[z])))));
+      } else {
+        for (int z = 0; z < R; ++z) {
+          const float o = __fsub_rn(k_.lmass[(m0 + z) * k_.nT + t], k_.lse[m0 + z]);
+          Q = __dadd_rn(Q, __dmul_rn(wz[z], static_cast<double>(
+                                                detexp32(__fadd_rn(tv[z * tstride], o)))));
+        }
+      }
+      const uint64_t Qi = quant40d(Q);
+      Rw = P > Qi ? P - Qi : 0;
+      (void)v;
+    };
+    const float* trow = k_.tls + m0 * V + v0;
+    if ((V & 3) == 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int v = 4 * sub + 32 * i;
+        if (v0 + v < V) {
+          const float4 p4 = *reinterpret_cast<const float4*>(prow + v);
+          float4 x4[RT > 0 ? RT : 1];
+          if constexpr (RT > 0) {
+            if (residual) {
+#pragma unroll
+              for (int z = 0; z < RT; ++z)
+                x4[z] = *reinterpret_cast<const float4*>(trow + z * V + v);
+            }
+          }
+          const float pe[4] = {p4.x, p4.y, p4.z, p4.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            uint64_t P, Rw;
+            if constexpr (RT > 0) {
+              float tv[RT];
+              if (residual) {
+#pragma unroll
+                for (int z = 0; z < RT; ++z)
+                  tv[z] = e == 0 ? x4[z].x : e == 1 ? x4[z].y : e == 2 ? x4[z].z : x4[z].w;
+              }
+              weights(v + e, pe[e], tv, 1, P, Rw);
+            } else {
+              weights(v + e, pe[e], trow + v + e, static_cast<int>(V), P, Rw);
+            }
+            sp += P;
+            sr += Rw;
+          }
+        }
+      }
+    } else {
+      for (int i = 0; i < 16; ++i) {
+        const int v = sub + 8 * i;
+        if (v0 + v < V) {
+          uint64_t P, Rw;
+          if constexpr (RT > 0) {
+            float tv[RT];
+            if (residual) {
+#pragma unroll
+              for (int z = 0; z < RT; ++z) tv[z] = trow[z * V + v];
+            }
+            weights(v, prow[v], tv, 1, P, Rw);
+          } else {
+            weights(v, prow[v], trow + v, static_cast<int>(V), P, Rw);
+          }
+          sp += P;
+          sr += Rw;
         }
       }
     }
-    sp = wave_sum_u64(sp);
-    sr = wave_sum_u64(sr);
-    if (lane == 0) {
-      a.p_tiles[b * k_.nT + t] = sp;
-      a.res_tiles[b * k_.nT + t] = sr;
-    }
+  }
+  sp += __shfl_xor(sp, 1);
+  sp += __shfl_xor(sp, 2);
+  sp += __shfl_xor(sp, 4);
+  sr += __shfl_xor(sr, 1);
+  sr += __shfl_xor(sr, 2);
+  sr += __shfl_xor(sr, 4);
+  if (sub == 0 && t < k_.nT) {
+    a.p_tiles[b * k_.nT + t] = sp;
+    a.res_tiles[b * k_.nT + t] = sr;
   }
 }
 
-__global__ __launch_bounds__(64) void finalize_kernel(VerifyArgs a, int nchunk) {
+// Per block: acceptance masses and E (binary64 sums of the chunk partials), then the residual
+// or bonus draw by inverse CDF over the tile sums (256 threads).
+__global__ __launch_bounds__(256) void finalize_kernel(VerifyArgs a, int nchunk) {
+  __shared__ double s_beta[kChainMaxK];
+  __shared__ uint64_t lds[8];
+  __shared__ double wz[kMaxR];
   const BlockArgs& k_ = a.blk;
   const int64_t b = blockIdx.x;
+  const int tid = threadIdx.x;
   const int lane = lane_id();
+  const int wave = tid >> 6;
+  const int K = static_cast<int>(k_.K);
   if (a.beta || a.exp_len) {
-    double prod = 1.0, E = 0.0;
-    for (int64_t k = 0; k < k_.K; ++k) {
-      const float* part = a.beta_part + (b * k_.K + k) * nchunk;
-      double s = 0.0;
-      for (int c = lane; c < nchunk; c += 64) s += static_cast<double>(part[c]);
-      s = wave_sum_f64(s);
-      if (a.beta && lane == 0) a.beta[b * k_.K + k] = static_cast<float>(s);
-      prod *= s;
-      E += prod;
+    for (int k0 = 0; k0 < K; k0 += kChainMaxK) {
+      const int kn = min(kChainMaxK, K - k0);
+      for (int kk = wave; kk < kn; kk += 4) {
+        const float* part = a.beta_part + (b * k_.K + k0 + kk) * nchunk;
+        double sum = 0.0;
+        for (int c = lane; c < nchunk; c += 64) sum += static_cast<double>(part[c]);
+        sum = wave_sum_f64(sum);
+        if (lane == 0) s_beta[kk] = sum;
+      }
+      __syncthreads();
+      for (int kk = tid; kk < kn; kk += blockDim.x)
+        if (a.beta) a.beta[b * k_.K + k0 + kk] = static_cast<float>(s_beta[kk]);
+      if (a.exp_len && tid == 0) {
+        // Running product and sum over all positions; kept in lds[7] / lds[6] across chunks.
+        double prod = k0 == 0 ? 1.0 : __longlong_as_double(static_cast<long long>(lds[7]));
+        double E = k0 == 0 ? 0.0 : __longlong_as_double(static_cast<long long>(lds[6]));
+        for (int kk = 0; kk < kn; ++kk) {
+          prod *= s_beta[kk];
+          E += prod;
+        }
+        lds[7] = static_cast<uint64_t>(__double_as_longlong(prod));
+        lds[6] = static_cast<uint64_t>(__double_as_longlong(E));
+        if (k0 + kn == K) a.exp_len[b] = static_cast<float>(E);
+      }
+      __syncthreads();
     }
-    if (a.exp_len && lane == 0) a.exp_len[b] = static_cast<float>(E);
   }
   if (a.trajectory) return;
   const int ks = a.n_accept[b];
   const bool residual = ks < k_.K;
   int tok = -1;
   if (residual || a.Kp == k_.K + 1) {
-    __shared__ double wz[kMaxR];
-    if (residual && lane < k_.R) wz[lane] = a.wpost[(b * k_.K + ks) * k_.R + lane];
+    if (residual && tid < k_.R) wz[tid] = a.wpost[(b * k_.K + ks) * k_.R + tid];
     __syncthreads();
     ResidualWeight W{k_.tls, k_.lmass, k_.lse, a.logp + (b * a.Kp + ks) * k_.V,
                      (b * k_.K + (residual ? ks : 0)) * k_.R, k_.V, k_.nT,
@@ -337,13 +440,13 @@ __global__ __launch_bounds__(64) void finalize_kernel(VerifyArgs a, int nchunk) 
     const uint32_t r = draw(k_.seed, kResidual, static_cast<uint32_t>(ks),
                             static_cast<uint64_t>(k_.seq_offset + b), k_.step);
     if (residual)
-      tok = select_by_tiles(a.res_tiles + b * k_.nT, k_.nT, k_.V, r,
-                            [&](int64_t v) { return W.res_int(v); });
+      tok = select_by_tiles_block(a.res_tiles + b * k_.nT, k_.nT, k_.V, r,
+                                  [&](int64_t v) { return W.res_int(v); }, lds);
     if (tok < 0)
-      tok = select_by_tiles(a.p_tiles + b * k_.nT, k_.nT, k_.V, r,
-                            [&](int64_t v) { return W.p_int(v); });
+      tok = select_by_tiles_block(a.p_tiles + b * k_.nT, k_.nT, k_.V, r,
+                                  [&](int64_t v) { return W.p_int(v); }, lds);
   }
-  if (lane == 0) a.next_token[b] = tok;
+  if (tid == 0) a.next_token[b] = tok;
 }
 
 }  // namespace
@@ -374,12 +477,19 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (!a.trajectory) {
-    hipLaunchKernelGGL(residual_kernel, dim3(static_cast<unsigned>(B), nchunk), dim3(256), 0,
-                       stream, a);
+    const dim3 grid(static_cast<unsigned>(B), nchunk);
+    switch (a.blk.R) {
+      case 1: hipLaunchKernelGGL(residual_kernel<1>, grid, dim3(256), 0, stream, a); break;
+      case 2: hipLaunchKernelGGL(residual_kernel<2>, grid, dim3(256), 0, stream, a); break;
+      case 4: hipLaunchKernelGGL(residual_kernel<4>, grid, dim3(256), 0, stream, a); break;
+      case 8: hipLaunchKernelGGL(residual_kernel<8>, grid, dim3(256), 0, stream, a); break;
+      case 16: hipLaunchKernelGGL(residual_kernel<16>, grid, dim3(256), 0, stream, a); break;
+      default: hipLaunchKernelGGL(residual_kernel<0>, grid, dim3(256), 0, stream, a); break;
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (want_beta || !a.trajectory) {
-    hipLaunchKernelGGL(finalize_kernel, dim3(static_cast<unsigned>(B)), dim3(64), 0, stream, a,
+    hipLaunchKernelGGL(finalize_kernel, dim3(static_cast<unsigned>(B)), dim3(256), 0, stream, a,
                        nchunk);
     e = hipGetLastError();
   }

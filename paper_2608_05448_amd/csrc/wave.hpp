@@ -138,4 +138,65 @@ __device__ __forceinline__ int select_by_tiles(const uint64_t* tiles, int nT, in
   return static_cast<int>(static_cast<int64_t>(tsel) * kTile + 2 * l + (pick0 ? 0 : 1));
 }
 
+// The same inverse-CDF selection done by a whole 256-thread workgroup (every thread calls it):
+// each thread sums a contiguous run of tile sums, a workgroup scan locates the run and then the
+// tile holding the threshold, and wavefront 0 scans that tile. `lds` must hold 8 uint64.
+template <class WeightFn>
+__device__ int select_by_tiles_block(const uint64_t* tiles, int nT, int64_t V, uint32_t r,
+                                     WeightFn weight, uint64_t* lds) {
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid >> 6;
+  const int per = (nT + 255) / 256;
+  const int t0 = min(nT, tid * per), t1 = min(nT, t0 + per);
+  uint64_t part = 0;
+  for (int t = t0; t < t1; ++t) part += tiles[t];
+  uint64_t incl = wave_incl_scan_u64(part);
+  if (lane == 63) lds[wave] = incl;
+  __syncthreads();
+  uint64_t base = 0, Z = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (w < wave) base += lds[w];
+    Z += lds[w];
+  }
+  __syncthreads();
+  if (Z == 0) return -1;
+  const uint64_t T = icdf_threshold(r, Z);
+  incl += base;
+  const uint64_t excl = incl - part;
+  if (excl <= T && T < incl) {  // exactly one thread's run holds the threshold
+    uint64_t c = excl;
+    for (int t = t0; t < t1; ++t) {
+      if (c + tiles[t] > T) {
+        lds[4] = static_cast<uint64_t>(t);
+        lds[5] = c;
+        break;
+      }
+      c += tiles[t];
+    }
+  }
+  __syncthreads();
+  const int tsel = static_cast<int>(lds[4]);
+  const uint64_t before = lds[5];
+  if (wave == 0) {
+    const int64_t v0 = static_cast<int64_t>(tsel) * kTile + 2 * lane;
+    const uint64_t q0 = v0 < V ? weight(v0) : 0;
+    const uint64_t q1 = v0 + 1 < V ? weight(v0 + 1) : 0;
+    const uint64_t in = wave_incl_scan_u64(q0 + q1);
+    const bool h0 = before + in - q1 > T, h1 = before + in > T;
+    const uint64_t hit = __ballot(h0 || h1);
+    const int l = hit ? __ffsll(static_cast<unsigned long long>(hit)) - 1 : 0;
+    const int pick0 = __shfl(static_cast<int>(h0), l);  // whole wavefront active
+    if (lane == 0)
+      lds[6] = hit ? static_cast<uint64_t>(static_cast<int64_t>(tsel) * kTile + 2 * l +
+                                           (pick0 ? 0 : 1))
+                   : ~0ull;
+  }
+  __syncthreads();
+  const uint64_t res = lds[6];
+  __syncthreads();
+  return res == ~0ull ? -1 : static_cast<int>(res);
+}
+
 }  // namespace dbl
