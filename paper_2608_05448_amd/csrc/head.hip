@@ -303,21 +303,26 @@ __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_kernel(
 // MFMA fragment reads are free of bank conflicts: ds_read_b128 serves 16 consecutive lanes per
 // cycle from 64 four-byte banks (256 B), so rows r, r + 4, r + 8, r + 12 of a 64-byte-row tile
 // must land their chunk in different 16-byte bank groups (measured with SQ_LDS_BANK_CONFLICT).
-template <int BK_, int S_, int BM_>
+template <int BK_, int S_, int BM_, int WM_>
 struct DmaCfg {
   static constexpr int BV = 256, BM = BM_, BK = BK_, S = S_;
-  static constexpr int kThreads = 256, WM = 2, TM = BM / 2, NCB = TM / 32, NRB = 4;
-  static constexpr int kWgPerCu = BM == 256 ? 1 : 2;     // co-resident workgroups per CU
+  // Waves: 2 along the vocabulary (one 128-id tile each) times WM along the branch rows.
+  static constexpr int WM = WM_, NW = 2 * WM, kThreads = 64 * NW;
+  static constexpr int TM = BM / WM, NCB = TM / 32, NRB = 4;
   static constexpr int CPR = BK / 8;                     // 16-byte chunks per row
   static constexpr int ROWB = BK * 2;                    // bytes per LDS row
   static constexpr int RPI = 64 / CPR;                   // rows per DMA instruction
-  static constexpr int A_INST = BV / RPI / 4;            // DMA instructions per wave, w rows
-  static constexpr int B_INST = BM / RPI / 4;            // DMA instructions per wave, h rows
+  static constexpr int A_INST = BV / RPI / NW;           // DMA instructions per wave, w rows
+  static constexpr int B_INST = BM / RPI / NW;           // DMA instructions per wave, h rows
   static constexpr int PER_STAGE = A_INST + B_INST;      // DMA instructions per wave per stage
   static constexpr int TBA = BV * ROWB;                  // bytes of the w tile of one stage
   static constexpr int TBB = BM * ROWB;                  // bytes of the h tile of one stage
+  // co-resident workgroups per CU (LDS-limited)
+  static constexpr int kWgPerCu = 2 * S * (TBA + TBB) <= 160 * 1024 ? 2 : 1;
   static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
   static_assert(BM == 128 || BM == 256, "branch-row tile of 128 or 256");
+  static_assert(WM == 2 || WM == 4, "2 or 4 waves along the branch rows");
+  static_assert(TM % 32 == 0 && A_INST >= 1 && B_INST >= 1, "wave tiling");
   static_assert(S >= 2 && S <= 5, "2 to 5 stages");
   static_assert((S - 2) * PER_STAGE <= 63, "vmcnt range");
   static_assert(S * (TBA + TBB) * kWgPerCu <= 160 * 1024, "LDS per CU");
@@ -354,10 +359,16 @@ __device__ __forceinline__ void wait_vmcnt() {
 #ifndef DBL_HEAD_STAGES
 #define DBL_HEAD_STAGES 4
 #endif
+#ifndef DBL_HEAD_FRAG_SLOTS
+#define DBL_HEAD_FRAG_SLOTS 8
+#endif
 #ifndef DBL_HEAD_BM
 #define DBL_HEAD_BM 256
 #endif
-using DCfg = DmaCfg<DBL_HEAD_BK, DBL_HEAD_STAGES, DBL_HEAD_BM>;
+#ifndef DBL_HEAD_WM
+#define DBL_HEAD_WM 2
+#endif
+using DCfg = DmaCfg<DBL_HEAD_BK, DBL_HEAD_STAGES, DBL_HEAD_BM, DBL_HEAD_WM>;
 
 template <class C>
 __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel(
@@ -443,9 +454,17 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
   constexpr int NF = C::NRB + C::NCB;         // fragments per k step
   constexpr int NQ = C::NRB * C::NCB;         // MFMAs per k step
   constexpr int NSLOT = NQ / 2;               // MFMA pairs per k step
-  static_assert(C::BK == 32, "the pipeline interleaves two 16-deep k steps per stage");
-  // Slot i of a k step issues MFMA pair i, then fragments [i NF / NSLOT, (i + 1) NF / NSLOT)
-  // and DMA instructions [i P / NSLOT, (i + 1) P / NSLOT).
+  constexpr int KS = C::BK / 16;              // 16-deep k steps per stage (2 or 4)
+  constexpr int FS = DBL_HEAD_FRAG_SLOTS < NSLOT ? DBL_HEAD_FRAG_SLOTS : NSLOT;
+  constexpr int DKS = KS - 1;                 // k steps that carry the stage's DMA
+  // MFMA q of a k step multiplies A block q / NCB by B block q % NCB, so fragments are
+  // loaded in the order they are first needed: A0, B0 .. B(NCB-1), A1 .. A(NRB-1).
+  auto frag_of = [](int f) { return f == 0 ? 0 : (f <= C::NCB ? C::NRB + f - 1 : f - C::NCB); };
+  // Slot i of a k step issues MFMA pair i, then the next k step's fragment loads
+  // [i NF / FS, (i + 1) NF / FS) (slots i < FS); the stage's DMA instructions are spread
+  // evenly over the slots of the first KS - 1 k steps. No load depends on a run-time
+  // condition, so the outstanding LDS reads are known at every MFMA and each waits only for
+  // its own operands.
 
   const int nk = d / C::BK;
   // Prologue: stages 0 .. S-2 in flight, stage 0 visible, its first-k-step fragments loaded.
@@ -456,7 +475,7 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
 #pragma unroll
     for (int i = 0; i < C::PER_STAGE; ++i) {
       if (j == 0) issue_one(std::integral_constant<int, 0>{}, kj, i);
-      if (j == 1) issue_one(std::integral_constant<int, 1>{}, kj, i);
+      if (j == 1) issue_one(std::integral_constant<int, 1 % C::S>{}, kj, i);
       if (j == 2) issue_one(std::integral_constant<int, 2 % C::S>{}, kj, i);
       if (j == 3) issue_one(std::integral_constant<int, 3 % C::S>{}, kj, i);
     }
@@ -465,12 +484,13 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 #pragma unroll
-  for (int i = 0; i < NF; ++i) load_frag(0, sA[0], sB[0], 0, i);
+  for (int f = 0; f < NF; ++f) load_frag(0, sA[0], sB[0], 0, frag_of(f));
 
-  // Iteration kt computes stage kt (slot kt % S). First half: k step 0 with fragment set 0,
-  // interleaved with the loads of k step 1 (set 1) and the DMA of stage kt + S - 1 into the
-  // slot of stage kt - 1. Then wait for stage kt + 1, barrier. Second half: k step 1, with
-  // the loads of stage kt + 1's first fragments (set 0).
+  // Iteration kt computes stage kt (slot kt % S) in KS k steps; k step s multiplies with
+  // fragment set s % 2 while loading set (s + 1) % 2 for k step s + 1. The DMA of stage
+  // kt + S - 1 goes to the slot of stage kt - 1 during the first KS - 1 k steps. Before the
+  // last k step: wait for stage kt + 1, barrier; the last k step then loads stage kt + 1's
+  // first fragments (set 0; after the last stage these read a slot that is never consumed).
   auto body = [&](auto j_c, int kt) {
     constexpr int j = decltype(j_c)::value;
     constexpr int jn = (j + 1) % C::S;            // slot of stage kt + 1
@@ -480,42 +500,51 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
     // stay unconditional, so the outstanding count per wave is always S - 2 stages.
     const int kd = min(kt + C::S - 1, nk - 1) * C::BK;
 #pragma unroll
-    for (int i = 0; i < NSLOT; ++i) {
-      mfma(0, 2 * i);
-      mfma(0, 2 * i + 1);
-#pragma unroll
-      for (int f = i * NF / NSLOT; f < (i + 1) * NF / NSLOT; ++f) load_frag(1, sA[j], sB[j], 1, f);
-#pragma unroll
-      for (int q = i * C::PER_STAGE / NSLOT; q < (i + 1) * C::PER_STAGE / NSLOT; ++q)
-        issue_one(std::integral_constant<int, jd>{}, kd, q);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    const bool next = kt + 1 < nk;
-    if (next) {
-      wait_vmcnt<(C::S - 2) * C::PER_STAGE>();
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      __builtin_amdgcn_s_barrier();
-      asm volatile("" ::: "memory");
-    }
-#pragma unroll
-    for (int i = 0; i < NSLOT; ++i) {
-      mfma(1, 2 * i);
-      mfma(1, 2 * i + 1);
-      if (next) {
-#pragma unroll
-        for (int f = i * NF / NSLOT; f < (i + 1) * NF / NSLOT; ++f)
-          load_frag(0, sA[jn], sB[jn], 0, f);
+    for (int st = 0; st < KS; ++st) {
+      const int cur = st & 1;
+      if (st == KS - 1) {
+        wait_vmcnt<(C::S - 2) * C::PER_STAGE>();
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
       }
-      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < NSLOT; ++i) {
+        mfma(cur, 2 * i);
+        mfma(cur, 2 * i + 1);
+        if (i < FS) {
+#pragma unroll
+          for (int f = i * NF / FS; f < (i + 1) * NF / FS; ++f) {
+            if (st < KS - 1)
+              load_frag(cur ^ 1, sA[j], sB[j], st + 1, frag_of(f));
+            else
+              load_frag(0, sA[jn], sB[jn], 0, frag_of(f));
+          }
+        }
+        if (st < DKS) {
+          constexpr int TS = DKS * NSLOT;
+          const int g = st * NSLOT + i;
+#pragma unroll
+          for (int q = g * C::PER_STAGE / TS; q < (g + 1) * C::PER_STAGE / TS; ++q)
+            issue_one(std::integral_constant<int, jd>{}, kd, q);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   };
-  for (int kt0 = 0; kt0 < nk; kt0 += C::S) {
+  int kt0 = 0;
+  for (; kt0 + C::S <= nk; kt0 += C::S) {
     body(std::integral_constant<int, 0>{}, kt0);
-    if (kt0 + 1 < nk) body(std::integral_constant<int, 1>{}, kt0 + 1);
-    if (C::S > 2 && kt0 + 2 < nk) body(std::integral_constant<int, 2 % C::S>{}, kt0 + 2);
-    if (C::S > 3 && kt0 + 3 < nk) body(std::integral_constant<int, 3 % C::S>{}, kt0 + 3);
-    if (C::S > 4 && kt0 + 4 < nk) body(std::integral_constant<int, 4 % C::S>{}, kt0 + 4);
+    body(std::integral_constant<int, 1>{}, kt0 + 1);
+    if constexpr (C::S > 2) body(std::integral_constant<int, 2 % C::S>{}, kt0 + 2);
+    if constexpr (C::S > 3) body(std::integral_constant<int, 3 % C::S>{}, kt0 + 3);
+    if constexpr (C::S > 4) body(std::integral_constant<int, 4 % C::S>{}, kt0 + 4);
   }
+  // Remaining nk % S stages.
+  if (kt0 < nk) body(std::integral_constant<int, 0>{}, kt0);
+  if (kt0 + 1 < nk) body(std::integral_constant<int, 1>{}, kt0 + 1);
+  if (C::S > 3 && kt0 + 2 < nk) body(std::integral_constant<int, 2 % C::S>{}, kt0 + 2);
+  if (C::S > 4 && kt0 + 3 < nk) body(std::integral_constant<int, 3 % C::S>{}, kt0 + 3);
 
   wait_vmcnt<0>();
 
