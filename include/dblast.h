@@ -18,6 +18,10 @@
  *   dbl_verify_block    sequential accept test, residual or bonus draw, acceptance mass
  *   dbl_expected_len    acceptance mass and expected accepted length along a given trajectory
  *
+ * and the same three steps for the greedy-branch proposal that the paper's reported
+ * experiments use (appendix "Greedy-Branch Proposal"): dbl_sample_greedy, dbl_verify_greedy,
+ * dbl_expected_len_greedy, which take the head's per-row argmax instead of log-probabilities.
+ *
  * Notation. B blocks (one per sequence), K drafted positions, R categories, d hidden size, V
  * vocabulary size. The paper writes b for the block length and K for the number of categories.
  * Row m of the branch hidden states and of every per-row output is m = (b*K + k)*R + r, and
@@ -87,7 +91,10 @@ typedef enum {
   DBL_OP_HEAD = 0,
   DBL_OP_SAMPLE = 1,
   DBL_OP_VERIFY = 2,
-  DBL_OP_EXPECTED_LEN = 3
+  DBL_OP_EXPECTED_LEN = 3,
+  DBL_OP_SAMPLE_GREEDY = 4,
+  DBL_OP_VERIFY_GREEDY = 5,
+  DBL_OP_EXPECTED_LEN_GREEDY = 6
 } dbl_op;
 
 typedef struct {
@@ -121,12 +128,17 @@ const char* dbl_last_error(void);
  *   h      [B, K, R, d] row-major, element type dt: branch hidden states h_{k,z}
  *   w      [V, d] row-major (the lm_head.weight layout; the math weight is w^T), type dt
  *   tls    out [M, V] fp32      lmass  out [M, nT] fp32      lse  out [M] fp32
- *   ws     workspace of dbl_workspace_bytes(DBL_OP_HEAD, shape) bytes (may be 0 and NULL)
+ *   argmax out [M] int32 or NULL: argmax_v logit[m, v], the lowest id among equal maxima
+ *          (the greedy branch tokens x_hat[k, z] of appendix "Greedy-Branch Proposal"); taken on
+ *          the same fp32 logits, so tls, lmass and lse are identical with or without it
+ *   ws     workspace of dbl_workspace_bytes(DBL_OP_HEAD, shape) bytes (M * 8); needed only
+ *          when argmax is requested, otherwise may be 0 and NULL
  * Errors: DBL_EINVAL for null pointers, DBL_EDTYPE for other dt, DBL_ESHAPE when d % 8 != 0
- * or a dimension is out of range.
+ * or a dimension is out of range, DBL_EWORKSPACE when argmax is requested without workspace.
  */
 dbl_status dbl_head_logprobs(dbl_shape shape, int dt, const void* h, const void* w, float* tls,
-                             float* lmass, float* lse, void* ws, size_t ws_bytes, void* stream);
+                             float* lmass, float* lse, int32_t* argmax, void* ws,
+                             size_t ws_bytes, void* stream);
 
 /*
  * dbl_sample_block - draw one block per sequence from the latent mixture (Sec. "Dependent
@@ -189,6 +201,62 @@ dbl_status dbl_expected_len(dbl_shape shape, const float* tls, const float* lmas
                             const float* lse, const float* prior_logits, float z_temp,
                             const int32_t* x, const float* logp, float* beta, float* exp_len,
                             void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Greedy-branch mode (appendix "Greedy-Branch Proposal", "Prefix-Marginalized Conditional",
+ * "Distributional Correctness"; Algorithm "Greedy-Branch Dependent Speculative Verification").
+ * Each category's branch is decoded greedily, x_hat[b, k, z] = argmax_v q_k(v | y, z) (the
+ * argmax output of dbl_head_logprobs, laid out [B, K, R] like the head rows), and the proposal
+ * is the mixture of these R deterministic blocks weighted by the prior q_{Z_T}. Verification
+ * uses its prefix-marginalised conditional
+ *     q(v | x_<k) = sum_{z in C_k} pi~_{k,z} 1{v = x_hat[b, k, z]},
+ *     C_k = {z : x_hat[b, j, z] = x_j for all j < k},  pi~_{k,z} = q_{Z_T}(z) / sum_{C_k} q_{Z_T},
+ * supported on at most R tokens, so no vocabulary row of the drafter is read. Draws and
+ * decisions follow the determinism contract above (pi~ is the log-domain normalisation of the
+ * prior restricted to C_k; q at a token is the ascending-z binary64 sum of the matching
+ * weights); there is no token draw (purpose 1 is unused). Ids in x_hat outside [0, V) are
+ * never proposed tokens.
+ */
+
+/*
+ * dbl_sample_greedy - draw z ~ q_{Z_T} per block and copy branch z: x[b, k] = x_hat[b, k, z].
+ *   x_hat   [B, K, R] int32 branch tokens;  prior_logits [B, R] fp32;  z_temp >= 0
+ *   z_out   out [B] int32;  x_out  out [B, K] int32 (-1 for a block whose prior has no
+ *           quantised mass)
+ * No workspace (dbl_workspace_bytes(DBL_OP_SAMPLE_GREEDY, .) = 0). shape.d is unused.
+ * Errors: DBL_EINVAL for null pointers or z_temp < 0 or NaN; DBL_ESHAPE.
+ */
+dbl_status dbl_sample_greedy(dbl_shape shape, const int32_t* x_hat, const float* prior_logits,
+                             float z_temp, uint64_t seed, uint64_t step, int64_t seq_offset,
+                             int32_t* z_out, int32_t* x_out, void* stream);
+
+/*
+ * dbl_verify_greedy - sequential verification of drafted blocks against the greedy-branch
+ * conditional: position k is accepted with probability min(1, p_k(x_k) / q(x_k | x_<k)) while
+ * all earlier positions were; the first rejection draws from norm(max(p_k - q(. | x_<k), 0))
+ * (from p_k if that has no quantised mass); full acceptance with Kp = K + 1 draws the bonus
+ * token from p_K. Arguments and outputs as dbl_verify_block, with x_hat [B, K, R] in place of
+ * the log-probability arrays; accept_mass is sum_v min(p_k(v), q(v | x_<k)) over the support.
+ * Workspace: dbl_workspace_bytes(DBL_OP_VERIFY_GREEDY, shape) bytes.
+ * Errors: as dbl_verify_block.
+ */
+dbl_status dbl_verify_greedy(dbl_shape shape, const int32_t* x_hat, const float* prior_logits,
+                             float z_temp, const int32_t* x, const float* logp, int64_t Kp,
+                             uint64_t seed, uint64_t step, int64_t seq_offset, int32_t* n_accept,
+                             int32_t* next_token, float* accept_mass, float* al_expected,
+                             float* exp_len, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * dbl_expected_len_greedy - beta_k = sum_v min(p_k(v), q(v | x_<k)) with the greedy-branch
+ * conditional along a given trajectory x [B, K], and E = sum_i prod_{j<=i} beta_j.
+ *   logp [B, K, V] fp32;  beta out [B, K] fp32 or NULL;  exp_len out [B] fp32
+ * Workspace: dbl_workspace_bytes(DBL_OP_EXPECTED_LEN_GREEDY, shape) bytes.
+ * Errors: as dbl_expected_len.
+ */
+dbl_status dbl_expected_len_greedy(dbl_shape shape, const int32_t* x_hat,
+                                   const float* prior_logits, float z_temp, const int32_t* x,
+                                   const float* logp, float* beta, float* exp_len, void* ws,
+                                   size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

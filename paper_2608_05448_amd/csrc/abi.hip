@@ -54,8 +54,22 @@ WsLayout layout(int op, const dbl_shape& s) {
   size_t sizes[4] = {0, 0, 0, 0};
   int n = 0;
   switch (op) {
-    case DBL_OP_HEAD:
+    case DBL_OP_HEAD:  // argmax keys, used only when argmax is requested
+      sizes[0] = B * K * R * sizeof(uint64_t);
+      n = 1;
+      break;
+    case DBL_OP_SAMPLE_GREEDY:
       n = 0;
+      break;
+    case DBL_OP_VERIFY_GREEDY:
+      sizes[0] = B * K * R * sizeof(double);
+      sizes[1] = B * nT * sizeof(uint64_t);
+      sizes[2] = B * nT * sizeof(uint64_t);
+      n = 3;
+      break;
+    case DBL_OP_EXPECTED_LEN_GREEDY:
+      sizes[0] = B * K * R * sizeof(double);
+      n = 1;
       break;
     case DBL_OP_SAMPLE:
       sizes[0] = B * K * nT * sizeof(uint64_t);
@@ -132,6 +146,23 @@ dbl_status check_block_inputs(const dbl_shape& s, const float* tls, const float*
   return ok();
 }
 
+dbl_status check_greedy_inputs(const dbl_shape& s, const int32_t* xhat, const float* prior,
+                               float z_temp) {
+  if (dbl_status st = check_shape(s, false)) return st;
+  if (!xhat || !prior) return fail(DBL_EINVAL, "NULL input pointer");
+  if (!(z_temp >= 0.0f) || isinf(z_temp))
+    return fail(DBL_EINVAL, "z_temp must be finite and >= 0");
+  return ok();
+}
+
+dbl::GreedyArgs greedy_args(const dbl_shape& s, const int32_t* xhat, const float* prior,
+                            float z_temp, uint64_t seed, uint64_t step, int64_t seq_offset) {
+  dbl::GreedyArgs a{};
+  a.blk = block_args(s, nullptr, nullptr, nullptr, prior, z_temp, seed, step, seq_offset);
+  a.xhat = xhat;
+  return a;
+}
+
 }  // namespace
 
 extern "C" {
@@ -160,13 +191,16 @@ const char* dbl_status_string(int status) {
 const char* dbl_last_error(void) { return g_last_error.c_str(); }
 
 dbl_status dbl_head_logprobs(dbl_shape s, int dt, const void* h, const void* w, float* tls,
-                             float* lmass, float* lse, void* ws, size_t ws_bytes, void* stream) {
+                             float* lmass, float* lse, int32_t* argmax, void* ws,
+                             size_t ws_bytes, void* stream) {
   if (dbl_status st = check_shape(s, true)) return st;
   if (dt != DBL_F32 && dt != DBL_BF16) return fail(DBL_EDTYPE, "dtype must be DBL_F32 or DBL_BF16");
   if (dt == DBL_BF16 && s.d % 8 != 0) return fail(DBL_ESHAPE, "bf16 head needs d % 8 == 0");
   if (!h || !w || !tls || !lmass || !lse) return fail(DBL_EINVAL, "NULL pointer");
   WsLayout L;
-  if (dbl_status st = check_ws(DBL_OP_HEAD, s, ws, ws_bytes, &L)) return st;
+  if (argmax) {
+    if (dbl_status st = check_ws(DBL_OP_HEAD, s, ws, ws_bytes, &L)) return st;
+  }
   if (s.B == 0) return ok();
   dbl::HeadArgs a;
   a.M = s.B * s.K * s.R;
@@ -178,6 +212,8 @@ dbl_status dbl_head_logprobs(dbl_shape s, int dt, const void* h, const void* w, 
   a.tls = tls;
   a.lmass = lmass;
   a.lse = lse;
+  a.argmax = argmax;
+  a.amax_keys = argmax ? reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + L.off[0]) : nullptr;
   return hip_status(dbl::launch_head(a, static_cast<hipStream_t>(stream)), "head launch");
 }
 
@@ -258,6 +294,71 @@ dbl_status dbl_expected_len(dbl_shape s, const float* tls, const float* lmass,
   a.p_tiles = nullptr;
   return hip_status(dbl::launch_verify(a, static_cast<hipStream_t>(stream)),
                     "expected_len launch");
+}
+
+dbl_status dbl_sample_greedy(dbl_shape s, const int32_t* x_hat, const float* prior_logits,
+                             float z_temp, uint64_t seed, uint64_t step, int64_t seq_offset,
+                             int32_t* z_out, int32_t* x_out, void* stream) {
+  if (dbl_status st = check_greedy_inputs(s, x_hat, prior_logits, z_temp)) return st;
+  if (!z_out || !x_out) return fail(DBL_EINVAL, "NULL output pointer");
+  if (s.B == 0) return ok();
+  dbl::GreedyArgs a = greedy_args(s, x_hat, prior_logits, z_temp, seed, step, seq_offset);
+  a.z_out = z_out;
+  a.x_out = x_out;
+  return hip_status(dbl::launch_sample_greedy(a, static_cast<hipStream_t>(stream)),
+                    "greedy sample launch");
+}
+
+dbl_status dbl_verify_greedy(dbl_shape s, const int32_t* x_hat, const float* prior_logits,
+                             float z_temp, const int32_t* x, const float* logp, int64_t Kp,
+                             uint64_t seed, uint64_t step, int64_t seq_offset, int32_t* n_accept,
+                             int32_t* next_token, float* accept_mass, float* al_expected,
+                             float* exp_len, void* ws, size_t ws_bytes, void* stream) {
+  if (dbl_status st = check_greedy_inputs(s, x_hat, prior_logits, z_temp)) return st;
+  if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
+  if (!n_accept || !next_token) return fail(DBL_EINVAL, "NULL output pointer");
+  if (Kp != s.K && Kp != s.K + 1) return fail(DBL_EINVAL, "Kp must be K or K + 1");
+  WsLayout L;
+  if (dbl_status st = check_ws(DBL_OP_VERIFY_GREEDY, s, ws, ws_bytes, &L)) return st;
+  if (s.B == 0) return ok();
+  char* base = static_cast<char*>(ws);
+  dbl::GreedyArgs a = greedy_args(s, x_hat, prior_logits, z_temp, seed, step, seq_offset);
+  a.x = x;
+  a.logp = logp;
+  a.Kp = Kp;
+  a.trajectory = false;
+  a.n_accept = n_accept;
+  a.next_token = next_token;
+  a.beta = accept_mass;
+  a.al = al_expected;
+  a.exp_len = exp_len;
+  a.wpost = reinterpret_cast<double*>(base + L.off[0]);
+  a.res_tiles = reinterpret_cast<uint64_t*>(base + L.off[1]);
+  a.p_tiles = reinterpret_cast<uint64_t*>(base + L.off[2]);
+  return hip_status(dbl::launch_verify_greedy(a, static_cast<hipStream_t>(stream)),
+                    "greedy verify launch");
+}
+
+dbl_status dbl_expected_len_greedy(dbl_shape s, const int32_t* x_hat,
+                                   const float* prior_logits, float z_temp, const int32_t* x,
+                                   const float* logp, float* beta, float* exp_len, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  if (dbl_status st = check_greedy_inputs(s, x_hat, prior_logits, z_temp)) return st;
+  if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
+  if (!exp_len) return fail(DBL_EINVAL, "NULL output pointer");
+  WsLayout L;
+  if (dbl_status st = check_ws(DBL_OP_EXPECTED_LEN_GREEDY, s, ws, ws_bytes, &L)) return st;
+  if (s.B == 0) return ok();
+  dbl::GreedyArgs a = greedy_args(s, x_hat, prior_logits, z_temp, 0, 0, 0);
+  a.x = x;
+  a.logp = logp;
+  a.Kp = s.K;
+  a.trajectory = true;
+  a.beta = beta;
+  a.exp_len = exp_len;
+  a.wpost = reinterpret_cast<double*>(static_cast<char*>(ws) + L.off[0]);
+  return hip_status(dbl::launch_verify_greedy(a, static_cast<hipStream_t>(stream)),
+                    "greedy expected_len launch");
 }
 
 }  // extern "C"

@@ -36,16 +36,25 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Argmax of a row across vocabulary tiles: every tile contributes the 64-bit key
+// (order-preserving bits of its maximum logit, ~id) through an atomic maximum, so the winner is
+// the largest logit and, among equal logits, the lowest id. -0 is folded into +0.
+__device__ __forceinline__ uint64_t argmax_key(float x, int64_t v) {
+  uint32_t u = __float_as_uint(x + 0.0f);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (static_cast<uint64_t>(u) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(v));
+}
+
 // Epilogue shared by the bf16 kernels. The wave holds the logits of one vocabulary tile (ids
 // v0w .. v0w + 127) for NCB * 32 branch rows. Lane l holds row m0w + 32 cb + l % 32 and, in
 // register r of row block rb, id v0w + 32 rb + 8 (r / 4) + 4 (l / 32) + r % 4. For each row:
 // tile max and sum of exponentials in registers plus one cross-half exchange, then the tile
 // log-mass and the tile-normalised log-probs are written; logits never reach memory.
-template <int NRB, int NCB>
+template <int NRB, int NCB, bool ARG>
 __device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], float* tls,
-                                                      float* lmass, int64_t M, int64_t V,
-                                                      int nT, int64_t v0w, int64_t m0w,
-                                                      int lane, int vec4) {
+                                                      float* lmass, uint64_t* amax, int64_t M,
+                                                      int64_t V, int nT, int64_t v0w,
+                                                      int64_t m0w, int lane, int vec4) {
   const int half = lane >> 5;
   const int t = static_cast<int>(v0w / kVTile);
   const int vlim = static_cast<int>(V - v0w < kVTile ? V - v0w : kVTile);  // ids in this tile
@@ -55,12 +64,31 @@ __device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], f
     const int64_t m = m0w + cb * 32 + (lane & 31);
     float mx = -INFINITY;
     float s = 0.0f;
+    int vi = 0;  // offset in the tile of this lane's first maximum (ARG only)
     if (full) {
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[rb][cb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+        for (int r = 0; r < 16; ++r) {
+          if constexpr (ARG) {
+            if (acc[rb][cb][r] > mx) {
+              mx = acc[rb][cb][r];
+              vi = rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+            }
+          } else {
+            mx = fmaxf(mx, acc[rb][cb][r]);
+          }
+        }
+      if constexpr (ARG) {
+        const float omx = __shfl_xor(mx, 32);
+        const int ovi = __shfl_xor(vi, 32);
+        if (omx > mx || (omx == mx && ovi < vi)) {
+          mx = omx;
+          vi = ovi;
+        }
+      } else {
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+      }
       const float nb = -mx * kLog2e;
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb)
@@ -70,9 +98,19 @@ __device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], f
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3) < vlim) mx = fmaxf(mx, acc[rb][cb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+        for (int r = 0; r < 16; ++r) {
+          const int o = rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          if (o < vlim && acc[rb][cb][r] > mx) {
+            mx = acc[rb][cb][r];
+            vi = o;
+          }
+        }
+      const float omx = __shfl_xor(mx, 32);
+      const int ovi = __shfl_xor(vi, 32);
+      if (omx > mx || (omx == mx && ovi < vi)) {
+        mx = omx;
+        vi = ovi;
+      }
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
@@ -84,6 +122,10 @@ __device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], f
     const float lm = mx + __logf(s);
     if (m < M) {
       if (half == 0) lmass[m * nT + t] = lm;
+      if constexpr (ARG) {
+        if (half == 0) atomicMax(reinterpret_cast<unsigned long long*>(amax + m),
+                                 static_cast<unsigned long long>(argmax_key(mx, v0w + vi)));
+      }
       float* row = tls + m * V + v0w + 4 * half;
       if (full && vec4) {
 #pragma unroll
@@ -163,10 +205,11 @@ __device__ __forceinline__ void tile_of(int L, int n_vtiles, int n_mtiles, int* 
   }
 }
 
-template <class C>
+template <class C, bool ARG>
 __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_kernel(
     const __bf16* __restrict__ h, const __bf16* __restrict__ w, float* __restrict__ tls,
-    float* __restrict__ lmass, int64_t M, int64_t V, int d, int nT, int n_mtiles, int vec4) {
+    float* __restrict__ lmass, uint64_t* __restrict__ amax, int64_t M, int64_t V, int d, int nT,
+    int n_mtiles, int vec4) {
   __shared__ __attribute__((aligned(16))) __bf16 As[2][C::BV * C::LDK];
   __shared__ __attribute__((aligned(16))) __bf16 Bs[2][C::BM * C::LDK];
 
@@ -291,8 +334,8 @@ __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_kernel(
 
   const int64_t v0w = v0 + wv * kVTile;
   if (v0w >= V) return;
-  tile_logsoftmax_store<C::NRB, C::NCB>(acc, tls, lmass, M, V, nT, v0w, m0 + wm * C::TM, lane,
-                                        vec4);
+  tile_logsoftmax_store<C::NRB, C::NCB, ARG>(acc, tls, lmass, amax, M, V, nT, v0w,
+                                             m0 + wm * C::TM, lane, vec4);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -370,10 +413,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 #endif
 using DCfg = DmaCfg<DBL_HEAD_BK, DBL_HEAD_STAGES, DBL_HEAD_BM, DBL_HEAD_WM>;
 
-template <class C>
+template <class C, bool ARG>
 __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel(
     const __bf16* __restrict__ h, const __bf16* __restrict__ w, float* __restrict__ tls,
-    float* __restrict__ lmass, int64_t M, int64_t V, int d, int nT, int n_mtiles, int vec4) {
+    float* __restrict__ lmass, uint64_t* __restrict__ amax, int64_t M, int64_t V, int d, int nT,
+    int n_mtiles, int vec4) {
   constexpr int TA = C::TBA, TB = C::TBB;
   __shared__ __attribute__((aligned(1024))) char sA0[TA], sB0[TB], sA1[TA], sB1[TB];
   __shared__ __attribute__((aligned(1024))) char sA2[C::S > 2 ? TA : 16], sB2[C::S > 2 ? TB : 16];
@@ -550,8 +594,8 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
 
   const int64_t v0w = v0 + wv * kVTile;
   if (v0w >= V) return;
-  tile_logsoftmax_store<C::NRB, C::NCB>(acc, tls, lmass, M, V, nT, v0w, m0 + wm * C::TM, lane,
-                                        vec4);
+  tile_logsoftmax_store<C::NRB, C::NCB, ARG>(acc, tls, lmass, amax, M, V, nT, v0w,
+                                             m0 + wm * C::TM, lane, vec4);
 }
 
 // fp32 path: workgroup (vocabulary tile t, 4 branch rows); thread j owns id 128 t + j.
@@ -561,10 +605,12 @@ constexpr int kF32DChunk = 512;
 __global__ __launch_bounds__(128) void head_f32_kernel(const float* __restrict__ h,
                                                        const float* __restrict__ w,
                                                        float* __restrict__ tls,
-                                                       float* __restrict__ lmass, int64_t M,
+                                                       float* __restrict__ lmass,
+                                                       uint64_t* __restrict__ amax, int64_t M,
                                                        int64_t V, int d, int nT) {
   __shared__ float hs[kF32Rows][kF32DChunk];
   __shared__ float red[2][kF32Rows];
+  __shared__ int redi[2][kF32Rows];
   const int t = blockIdx.x;
   const int64_t m0 = static_cast<int64_t>(blockIdx.y) * kF32Rows;
   const int j = threadIdx.x;
@@ -599,6 +645,19 @@ __global__ __launch_bounds__(128) void head_f32_kernel(const float* __restrict__
     __syncthreads();
     mx = fmaxf(red[0][r], red[1][r]);
     __syncthreads();
+    if (amax) {  // first id of the tile holding the maximum
+      int first = valid && acc[r] == mx ? j : kVTile;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o));
+      if ((j & 63) == 0) redi[wave][r] = first;
+      __syncthreads();
+      first = min(redi[0][r], redi[1][r]);
+      const int64_t m = m0 + r;
+      if (j == 0 && m < M && first < kVTile)
+        atomicMax(reinterpret_cast<unsigned long long*>(amax + m),
+                  static_cast<unsigned long long>(argmax_key(mx, static_cast<int64_t>(t) * kVTile + first)));
+      __syncthreads();
+    }
     float s = wave_sum(valid ? __expf(acc[r] - mx) : 0.0f);
     if ((j & 63) == 0) red[wave][r] = s;
     __syncthreads();
@@ -613,10 +672,19 @@ __global__ __launch_bounds__(128) void head_f32_kernel(const float* __restrict__
   }
 }
 
-// lse[m] = log sum_t exp(lmass[m, t]); one wave per row.
+// Clears the per-row argmax keys before the head kernel accumulates into them.
+__global__ __launch_bounds__(256) void zero_u64_kernel(uint64_t* __restrict__ p, int64_t n) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+// lse[m] = log sum_t exp(lmass[m, t]); one wave per row. With argmax requested, also decodes
+// the row's winning key into the vocabulary id.
 __global__ __launch_bounds__(256) void lse_finalize_kernel(const float* __restrict__ lmass,
-                                                           float* __restrict__ lse, int64_t M,
-                                                           int nT) {
+                                                           float* __restrict__ lse,
+                                                           const uint64_t* __restrict__ amax,
+                                                           int32_t* __restrict__ argmax,
+                                                           int64_t M, int nT) {
   const int64_t m = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (m >= M) return;
@@ -636,45 +704,68 @@ __global__ __launch_bounds__(256) void lse_finalize_kernel(const float* __restri
   const float gmx = wave_max(mx);
   s = mx > -INFINITY ? s * __expf(mx - gmx) : 0.0f;
   s = wave_sum(s);
-  if (lane == 0) lse[m] = gmx + __logf(s);
+  if (lane == 0) {
+    lse[m] = gmx + __logf(s);
+    if (argmax) {
+      const uint64_t key = amax[m];
+      argmax[m] = key ? static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(key)) : -1;
+    }
+  }
 }
 
 }  // namespace
 
 hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
   const int nT = static_cast<int>((a.V + kVTile - 1) / kVTile);
+  uint64_t* amax = a.argmax ? a.amax_keys : nullptr;
+  if (amax) {
+    const int64_t zb = (a.M + 255) / 256;
+    if (zb > 0x7fffffff) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(zero_u64_kernel, dim3(static_cast<unsigned>(zb)), dim3(256), 0, stream,
+                       amax, a.M);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (a.dtype_bf16) {
     const int n_mtiles = static_cast<int>((a.M + Cfg::BM - 1) / Cfg::BM);
     const int64_t n_vtiles = (a.V + Cfg::BV - 1) / Cfg::BV;
     const int64_t nwg = n_vtiles * n_mtiles;
     if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
     const int vec4 = (a.V % 4 == 0) ? 1 : 0;
+    const __bf16* h = static_cast<const __bf16*>(a.h);
+    const __bf16* w = static_cast<const __bf16*>(a.w);
     if (a.d % DCfg::BK == 0) {
       const int dm = static_cast<int>((a.M + DCfg::BM - 1) / DCfg::BM);
       const int64_t dwg = ((a.V + DCfg::BV - 1) / DCfg::BV) * dm;
       if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
-      hipLaunchKernelGGL(head_bf16_dma_kernel<DCfg>, dim3(static_cast<unsigned>(dwg)),
-                         dim3(DCfg::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
-                         static_cast<const __bf16*>(a.w), a.tls, a.lmass, a.M, a.V, a.d, nT, dm,
-                         vec4);
+      const dim3 grid(static_cast<unsigned>(dwg)), block(DCfg::kThreads);
+      if (amax)
+        hipLaunchKernelGGL((head_bf16_dma_kernel<DCfg, true>), grid, block, 0, stream, h, w,
+                           a.tls, a.lmass, amax, a.M, a.V, a.d, nT, dm, vec4);
+      else
+        hipLaunchKernelGGL((head_bf16_dma_kernel<DCfg, false>), grid, block, 0, stream, h, w,
+                           a.tls, a.lmass, amax, a.M, a.V, a.d, nT, dm, vec4);
     } else {
-      hipLaunchKernelGGL(head_bf16_kernel<Cfg>, dim3(static_cast<unsigned>(nwg)),
-                         dim3(Cfg::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
-                         static_cast<const __bf16*>(a.w), a.tls, a.lmass, a.M, a.V, a.d, nT,
-                         n_mtiles, vec4);
+      const dim3 grid(static_cast<unsigned>(nwg)), block(Cfg::kThreads);
+      if (amax)
+        hipLaunchKernelGGL((head_bf16_kernel<Cfg, true>), grid, block, 0, stream, h, w, a.tls,
+                           a.lmass, amax, a.M, a.V, a.d, nT, n_mtiles, vec4);
+      else
+        hipLaunchKernelGGL((head_bf16_kernel<Cfg, false>), grid, block, 0, stream, h, w, a.tls,
+                           a.lmass, amax, a.M, a.V, a.d, nT, n_mtiles, vec4);
     }
   } else {
     const int64_t mblocks = (a.M + kF32Rows - 1) / kF32Rows;
     if (mblocks > 65535) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(head_f32_kernel, dim3(nT, static_cast<unsigned>(mblocks)), dim3(128), 0,
                        stream, static_cast<const float*>(a.h), static_cast<const float*>(a.w),
-                       a.tls, a.lmass, a.M, a.V, a.d, nT);
+                       a.tls, a.lmass, amax, a.M, a.V, a.d, nT);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t lse_blocks = (a.M + 3) / 4;
   hipLaunchKernelGGL(lse_finalize_kernel, dim3(static_cast<unsigned>(lse_blocks)), dim3(256), 0,
-                     stream, a.lmass, a.lse, a.M, nT);
+                     stream, a.lmass, a.lse, amax, amax ? a.argmax : nullptr, a.M, nT);
   return hipGetLastError();
 }
 

@@ -19,6 +19,8 @@ struct HeadArgs {
   float* tls;
   float* lmass;
   float* lse;
+  int32_t* argmax;      // [M] or null: lowest-index argmax of each row's logits
+  uint64_t* amax_keys;  // workspace [M] when argmax is requested
 };
 
 // The branch log-probabilities and block description shared by the sampler and verifier.
@@ -58,10 +60,33 @@ struct VerifyArgs {
   uint64_t* p_tiles;    // workspace [B, nT]
 };
 
+// Greedy-branch mode: the branch tokens replace the branch log-probabilities (blk.tls, lmass and
+// lse are unused).
+struct GreedyArgs {
+  BlockArgs blk;
+  const int32_t* xhat;  // [B, K, R] branch tokens argmax_v q_k(v | z)
+  int32_t* z_out;       // sample: [B]
+  int32_t* x_out;       // sample: [B, K]
+  const int32_t* x;     // verify: [B, K] draft or trajectory
+  const float* logp;    // verify: [B, Kp, V]
+  int64_t Kp;
+  bool trajectory;
+  int32_t* n_accept;
+  int32_t* next_token;
+  float* beta;
+  float* al;
+  float* exp_len;
+  double* wpost;        // workspace [B, K, R]
+  uint64_t* res_tiles;  // workspace [B, nT]
+  uint64_t* p_tiles;    // workspace [B, nT]
+};
+
 inline int n_chunks(int nT) { return (nT + kTilesPerChunk - 1) / kTilesPerChunk; }
 
 hipError_t launch_head(const HeadArgs& a, hipStream_t stream);
 hipError_t launch_sample(const SampleArgs& a, hipStream_t stream);
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
+hipError_t launch_sample_greedy(const GreedyArgs& a, hipStream_t stream);
+hipError_t launch_verify_greedy(const GreedyArgs& a, hipStream_t stream);
 
 }  // namespace dbl

@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(_HERE, "libdblast.so")
 
 DBL_OK, DBL_EINVAL, DBL_ESHAPE, DBL_EDTYPE, DBL_EWORKSPACE, DBL_EHIP = range(6)
 DBL_F32, DBL_BF16 = 0, 1
-DBL_OP_HEAD, DBL_OP_SAMPLE, DBL_OP_VERIFY, DBL_OP_EXPECTED_LEN = range(4)
+(DBL_OP_HEAD, DBL_OP_SAMPLE, DBL_OP_VERIFY, DBL_OP_EXPECTED_LEN, DBL_OP_SAMPLE_GREEDY,
+ DBL_OP_VERIFY_GREEDY, DBL_OP_EXPECTED_LEN_GREEDY) = range(7)
 VTILE = 128
 
 
@@ -45,12 +46,17 @@ _SIGS = {
     "dbl_workspace_bytes": (_SZ, [ctypes.c_int, Shape]),
     "dbl_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "dbl_last_error": (ctypes.c_char_p, []),
-    "dbl_head_logprobs": (ctypes.c_int, [Shape, ctypes.c_int, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dbl_head_logprobs": (ctypes.c_int, [Shape, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                                         _P]),
     "dbl_sample_block": (ctypes.c_int, [Shape, _P, _P, _P, _P, _F, _U64, _U64, _I64, _P, _P, _P,
                                         _SZ, _P]),
     "dbl_verify_block": (ctypes.c_int, [Shape, _P, _P, _P, _P, _F, _P, _P, _I64, _U64, _U64, _I64,
                                         _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "dbl_expected_len": (ctypes.c_int, [Shape, _P, _P, _P, _P, _F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dbl_sample_greedy": (ctypes.c_int, [Shape, _P, _P, _F, _U64, _U64, _I64, _P, _P, _P]),
+    "dbl_verify_greedy": (ctypes.c_int, [Shape, _P, _P, _F, _P, _P, _I64, _U64, _U64, _I64, _P,
+                                         _P, _P, _P, _P, _P, _SZ, _P]),
+    "dbl_expected_len_greedy": (ctypes.c_int, [Shape, _P, _P, _F, _P, _P, _P, _P, _P, _SZ, _P]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -119,10 +125,12 @@ def _workspace(op, shape, device, ws=None):
     return torch.empty(n, dtype=torch.uint8, device=device), n
 
 
-def dbl_head_logprobs(h, w, tls=None, lmass=None, lse=None):
+def dbl_head_logprobs(h, w, tls=None, lmass=None, lse=None, argmax=None, ws=None):
     """Branch log-probabilities for h [B, K, R, d] and w [V, d] (bf16 or fp32).
 
-    Returns (tls [B, K, R, V], lmass [B, K, R, nT], lse [B, K, R]) fp32 on the device.
+    Returns (tls [B, K, R, V], lmass [B, K, R, nT], lse [B, K, R]) fp32 on the device; with
+    ``argmax`` (True, or an int32 [B, K, R] tensor to fill) also the per-row argmax (the greedy
+    branch tokens) as a fourth element.
     """
     if h.dtype not in (torch.bfloat16, torch.float32):
         raise TypeError("h must be bfloat16 or float32")
@@ -139,11 +147,18 @@ def dbl_head_logprobs(h, w, tls=None, lmass=None, lse=None):
     _need(lmass, "lmass", torch.float32, (B, K, R, nT))
     _need(lse, "lse", torch.float32, (B, K, R))
     shape = Shape(B, K, R, d, V)
-    ws, nws = _workspace(DBL_OP_HEAD, shape, dev)
+    want_arg = argmax is not None and argmax is not False
+    if want_arg:
+        if argmax is True:
+            argmax = torch.empty((B, K, R), dtype=torch.int32, device=dev)
+        _need(argmax, "argmax", torch.int32, (B, K, R))
+        ws, nws = _workspace(DBL_OP_HEAD, shape, dev, ws)
+    else:
+        argmax, ws, nws = None, None, 0
     dt = DBL_BF16 if h.dtype == torch.bfloat16 else DBL_F32
     _check(load().dbl_head_logprobs(shape, dt, _ptr(h), _ptr(w), _ptr(tls), _ptr(lmass),
-                                    _ptr(lse), _ptr(ws), nws, _stream(dev)))
-    return tls, lmass, lse
+                                    _ptr(lse), _ptr(argmax), _ptr(ws), nws, _stream(dev)))
+    return (tls, lmass, lse, argmax) if want_arg else (tls, lmass, lse)
 
 
 def _block_shape(tls, lmass, lse, prior_logits):
@@ -221,4 +236,78 @@ def dbl_expected_len(tls, lmass, lse, prior_logits, x, logp, z_temp=1.0, want_be
     _check(load().dbl_expected_len(shape, _ptr(tls), _ptr(lmass), _ptr(lse), _ptr(prior_logits),
                                    float(z_temp), _ptr(x), _ptr(logp), _ptr(beta), _ptr(exp_len),
                                    _ptr(ws), nws, _stream(dev)))
+    return beta, exp_len
+
+
+def _greedy_shape(x_hat, prior_logits, V):
+    B, K, R = x_hat.shape
+    _need(x_hat, "x_hat", torch.int32)
+    _need(prior_logits, "prior_logits", torch.float32, (B, R))
+    return Shape(B, K, R, 0, int(V))
+
+
+def dbl_sample_greedy(x_hat, prior_logits, z_temp=1.0, seed=0, step=0, seq_offset=0, V=1,
+                      z_out=None, x_out=None):
+    """Greedy-branch draw from branch tokens x_hat [B, K, R]: returns (z [B], x [B, K]) int32.
+    ``V`` is only used for shape validation (the draw reads no vocabulary row)."""
+    shape = _greedy_shape(x_hat, prior_logits, V)
+    dev = x_hat.device
+    z_out = torch.empty(shape.B, dtype=torch.int32, device=dev) if z_out is None else z_out
+    x_out = torch.empty((shape.B, shape.K), dtype=torch.int32, device=dev) if x_out is None else x_out
+    _need(z_out, "z_out", torch.int32, (shape.B,))
+    _need(x_out, "x_out", torch.int32, (shape.B, shape.K))
+    _check(load().dbl_sample_greedy(shape, _ptr(x_hat), _ptr(prior_logits), float(z_temp),
+                                    int(seed), int(step), int(seq_offset), _ptr(z_out),
+                                    _ptr(x_out), _stream(dev)))
+    return z_out, x_out
+
+
+def dbl_verify_greedy(x_hat, prior_logits, x, logp, z_temp=1.0, seed=0, step=0, seq_offset=0,
+                      want_beta=True, want_al=True, want_exp_len=True, out=None, ws=None):
+    """Verify drafted blocks x [B, K] against logp [B, Kp, V] with the greedy-branch conditional
+    of branch tokens x_hat [B, K, R]; returns the same dict as ``dbl_verify_block``."""
+    if logp.dim() != 3:
+        raise ValueError("logp must be [B, Kp, V]")
+    shape = _greedy_shape(x_hat, prior_logits, logp.shape[2])
+    dev = x_hat.device
+    B, K = shape.B, shape.K
+    _need(x, "x", torch.int32, (B, K))
+    if logp.shape[0] != B:
+        raise ValueError("logp must be [B, Kp, V]")
+    _need(logp, "logp", torch.float32)
+    Kp = logp.shape[1]
+    o = {} if out is None else dict(out)
+    o.setdefault("n_accept", torch.empty(B, dtype=torch.int32, device=dev))
+    o.setdefault("next_token", torch.empty(B, dtype=torch.int32, device=dev))
+    if want_beta:
+        o.setdefault("accept_mass", torch.empty((B, K), dtype=torch.float32, device=dev))
+    if want_al:
+        o.setdefault("al_expected", torch.empty(B, dtype=torch.float32, device=dev))
+    if want_exp_len:
+        o.setdefault("exp_len", torch.empty(B, dtype=torch.float32, device=dev))
+    ws, nws = _workspace(DBL_OP_VERIFY_GREEDY, shape, dev, ws)
+    _check(load().dbl_verify_greedy(shape, _ptr(x_hat), _ptr(prior_logits), float(z_temp),
+                                    _ptr(x), _ptr(logp), int(Kp), int(seed), int(step),
+                                    int(seq_offset), _ptr(o["n_accept"]), _ptr(o["next_token"]),
+                                    _ptr(o.get("accept_mass")), _ptr(o.get("al_expected")),
+                                    _ptr(o.get("exp_len")), _ptr(ws), nws, _stream(dev)))
+    return o
+
+
+def dbl_expected_len_greedy(x_hat, prior_logits, x, logp, z_temp=1.0, want_beta=True, beta=None,
+                            exp_len=None, ws=None):
+    """Acceptance masses and expected accepted length along trajectories x [B, K] under the
+    greedy-branch conditional of x_hat [B, K, R]."""
+    shape = _greedy_shape(x_hat, prior_logits, logp.shape[-1])
+    dev = x_hat.device
+    B, K, V = shape.B, shape.K, shape.V
+    _need(x, "x", torch.int32, (B, K))
+    _need(logp, "logp", torch.float32, (B, K, V))
+    if want_beta and beta is None:
+        beta = torch.empty((B, K), dtype=torch.float32, device=dev)
+    exp_len = torch.empty(B, dtype=torch.float32, device=dev) if exp_len is None else exp_len
+    ws, nws = _workspace(DBL_OP_EXPECTED_LEN_GREEDY, shape, dev, ws)
+    _check(load().dbl_expected_len_greedy(shape, _ptr(x_hat), _ptr(prior_logits), float(z_temp),
+                                          _ptr(x), _ptr(logp), _ptr(beta), _ptr(exp_len),
+                                          _ptr(ws), nws, _stream(dev)))
     return beta, exp_len

@@ -46,7 +46,12 @@ def test_constants_and_status_strings(lib):
 def test_workspace_sizes(lib):
     S = D.Shape
     SIZE_MAX = ctypes.c_size_t(-1).value
-    assert lib.dbl_workspace_bytes(D.DBL_OP_HEAD, S(16, 16, 8, 4096, 151936)) == 0
+    # Head: one uint64 argmax key per row (used only when the argmax is requested).
+    assert lib.dbl_workspace_bytes(D.DBL_OP_HEAD, S(16, 16, 8, 4096, 151936)) == 2048 * 8
+    assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE_GREEDY, S(16, 16, 8, 0, 151936)) == 0
+    g = lib.dbl_workspace_bytes(D.DBL_OP_VERIFY_GREEDY, S(16, 16, 8, 0, 151936))
+    assert g == 2048 * 8 + 2 * -(-16 * 1187 * 8 // 256) * 256
+    assert lib.dbl_workspace_bytes(D.DBL_OP_EXPECTED_LEN_GREEDY, S(16, 16, 8, 0, 151936)) == 2048 * 8
     # Sample: one uint64 per (position, tile).
     assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, S(16, 16, 8, 0, 151936)) == \
         -(-16 * 16 * 1187 * 8 // 256) * 256
@@ -72,19 +77,58 @@ def test_head_validation(lib):
     S = D.Shape
     h, w, t, lm, ls = _fake(5)
     null = ctypes.c_void_p(None)
-    assert lib.dbl_head_logprobs(S(1, 4, 2, 60, 256), D.DBL_BF16, h, w, t, lm, ls, null, 0,
-                                 null) == D.DBL_ESHAPE
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 60, 256), D.DBL_BF16, h, w, t, lm, ls, null, null,
+                                 0, null) == D.DBL_ESHAPE
     assert "d % 8" in _err(lib)
-    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 256), 7, h, w, t, lm, ls, null, 0,
-                                 null) == D.DBL_EDTYPE
-    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 256), D.DBL_F32, null, w, t, lm, ls, null, 0,
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 256), 7, h, w, t, lm, ls, null, null,
+                                 0, null) == D.DBL_EDTYPE
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 256), D.DBL_F32, null, w, t, lm, ls, null, null,
+                                 0, null) == D.DBL_EINVAL
+    assert lib.dbl_head_logprobs(S(1, 0, 2, 64, 256), D.DBL_F32, h, w, t, lm, ls, null, null,
+                                 0, null) == D.DBL_ESHAPE
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 1 << 24), D.DBL_F32, h, w, t, lm, ls, null, null,
+                                 0, null) == D.DBL_ESHAPE
+    assert lib.dbl_head_logprobs(S(-1, 4, 2, 64, 256), D.DBL_F32, h, w, t, lm, ls, null, null,
+                                 0, null) == D.DBL_ESHAPE
+
+
+def test_head_argmax_needs_workspace(lib):
+    S = D.Shape
+    h, w, t, lm, ls, am = _fake(6)
+    null = ctypes.c_void_p(None)
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 256), D.DBL_F32, h, w, t, lm, ls, am, null, 0,
+                                 null) == D.DBL_EWORKSPACE
+    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 256), D.DBL_F32, h, w, t, lm, ls, am,
+                                 ctypes.c_void_p(0x100000), 8 * 8 - 1, null) == D.DBL_EWORKSPACE
+
+
+def test_greedy_validation(lib):
+    S = D.Shape
+    p = _fake(10)
+    null = ctypes.c_void_p(None)
+    shape = S(2, 4, 3, 0, 300)
+    aligned = ctypes.c_void_p(0x100000)
+    for zt in (-0.5, float("nan"), float("inf")):
+        assert lib.dbl_sample_greedy(shape, p[0], p[1], zt, 0, 0, 0, p[2], p[3],
+                                     null) == D.DBL_EINVAL
+    assert lib.dbl_sample_greedy(shape, null, p[1], 1.0, 0, 0, 0, p[2], p[3],
                                  null) == D.DBL_EINVAL
-    assert lib.dbl_head_logprobs(S(1, 0, 2, 64, 256), D.DBL_F32, h, w, t, lm, ls, null, 0,
+    assert lib.dbl_sample_greedy(S(2, 4, 65, 0, 300), p[0], p[1], 1.0, 0, 0, 0, p[2], p[3],
                                  null) == D.DBL_ESHAPE
-    assert lib.dbl_head_logprobs(S(1, 4, 2, 64, 1 << 24), D.DBL_F32, h, w, t, lm, ls, null, 0,
-                                 null) == D.DBL_ESHAPE
-    assert lib.dbl_head_logprobs(S(-1, 4, 2, 64, 256), D.DBL_F32, h, w, t, lm, ls, null, 0,
-                                 null) == D.DBL_ESHAPE
+    vws = lib.dbl_workspace_bytes(D.DBL_OP_VERIFY_GREEDY, shape)
+    for kp in (3, 6):
+        assert lib.dbl_verify_greedy(shape, p[0], p[1], 1.0, p[2], p[3], kp, 0, 0, 0, p[4], p[5],
+                                     null, null, null, aligned, vws, null) == D.DBL_EINVAL
+    assert lib.dbl_verify_greedy(shape, p[0], p[1], 1.0, p[2], p[3], 4, 0, 0, 0, p[4], p[5],
+                                 null, null, null, aligned, vws - 1, null) == D.DBL_EWORKSPACE
+    ews = lib.dbl_workspace_bytes(D.DBL_OP_EXPECTED_LEN_GREEDY, shape)
+    assert lib.dbl_expected_len_greedy(shape, p[0], p[1], 1.0, p[2], p[3], null, null, aligned,
+                                       ews, null) == D.DBL_EINVAL
+    # empty batch
+    assert lib.dbl_sample_greedy(S(0, 4, 3, 0, 300), p[0], p[1], 1.0, 0, 0, 0, p[2], p[3],
+                                 null) == D.DBL_OK
+    assert lib.dbl_verify_greedy(S(0, 4, 3, 0, 300), p[0], p[1], 1.0, p[2], p[3], 4, 0, 0, 0,
+                                 p[4], p[5], null, null, null, null, 0, null) == D.DBL_OK
 
 
 def test_sample_and_verify_validation(lib):
