@@ -1,12 +1,15 @@
 """Throughput of the DBLast head + block draw + verification on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen3_8b]
-                    [--temperature T] [--no-cpu-baseline] [--copy-calibration BYTES]
+                    [--temperature T] [--mode soft|greedy] [--no-cpu-baseline]
+                    [--copy-calibration BYTES]
 
 One step is one pass of the whole hot path over one batch of synthetic inputs already resident
 in HBM: dbl_head_logprobs (bf16 head GEMM + per-tile log-softmax), dbl_sample_block (category
 and token draw) and dbl_verify_block (posterior, accept test, residual/bonus draw, acceptance
 masses, AL_b and E). The Philox step counter advances every step. Prints one JSON line.
+With --mode greedy the step is the greedy-branch variant: the head also returns each row's
+argmax, then dbl_sample_greedy and dbl_verify_greedy.
 
 The metric is verified block positions per second, B*K / step time. The roofline entry is for
 the dominant kernel, the head GEMM: 2*M*d*V flops per launch over its average launch time,
@@ -52,12 +55,13 @@ def _traffic(workload: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-def _cpu_baseline(wl, h, w, ell, logp, budget_s: float):
+def _cpu_baseline(wl, h, w, ell, logp, budget_s: float, mode: str = "soft"):
     """The oracle on as many whole blocks as fit the time budget (at least one)."""
     import numpy as np
     import torch
     from threadpoolctl import threadpool_info
 
+    from oracle import greedy as GR
     from oracle import head as OH
     from oracle import mixture as MX
 
@@ -69,11 +73,18 @@ def _cpu_baseline(wl, h, w, ell, logp, budget_s: float):
     t0 = time.perf_counter()
     done = 0
     for b in range(wl.B):
-        tls, lm, ls = OH.head_factored(hh[b].reshape(K * R, d), ww, v_chunk=8192)
-        lq = OH.flat_logq(tls, lm, ls).reshape(1, K, R, V)
         seq = np.array([b])
-        _, x = MX.sample_blocks(lq, ee[b:b + 1], wl.z_temp, wl.philox_seed, 0, seq)
-        MX.verify_blocks(lq, ee[b:b + 1], wl.z_temp, x, lp[b:b + 1], wl.philox_seed, 0, seq)
+        if mode == "greedy":
+            logits = OH.head_logits(hh[b].reshape(K * R, d), ww)
+            xhat = GR.branch_tokens(logits).reshape(1, K, R)
+            _, x = GR.sample_blocks_greedy(xhat, ee[b:b + 1], wl.z_temp, wl.philox_seed, 0, seq)
+            GR.verify_blocks_greedy(xhat, ee[b:b + 1], wl.z_temp, x, lp[b:b + 1],
+                                    wl.philox_seed, 0, seq)
+        else:
+            tls, lm, ls = OH.head_factored(hh[b].reshape(K * R, d), ww, v_chunk=8192)
+            lq = OH.flat_logq(tls, lm, ls).reshape(1, K, R, V)
+            _, x = MX.sample_blocks(lq, ee[b:b + 1], wl.z_temp, wl.philox_seed, 0, seq)
+            MX.verify_blocks(lq, ee[b:b + 1], wl.z_temp, x, lp[b:b + 1], wl.philox_seed, 0, seq)
         done += 1
         if time.perf_counter() - t0 >= budget_s:
             break
@@ -82,8 +93,9 @@ def _cpu_baseline(wl, h, w, ell, logp, budget_s: float):
     cores = len(os.sched_getaffinity(0))
     return {"value": done * K / el, "unit": "positions/s", "cores": min(threads, cores),
             "kind": "oracle",
-            "sample": f"{done} of {wl.B} blocks ({done * K} positions): binary64 head, block draw "
-                      f"and verification, {el:.1f} s on the host"}
+            "sample": f"{done} of {wl.B} blocks ({done * K} positions): binary64 head, "
+                      f"{'greedy-branch ' if mode == 'greedy' else ''}block draw and "
+                      f"verification, {el:.1f} s on the host"}
 
 
 def _pmc_mean(csv_dir: str, counter: str, name_re: str) -> float:
@@ -143,6 +155,7 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3_8b")
     ap.add_argument("--temperature", type=float, default=None)
+    ap.add_argument("--mode", choices=("soft", "greedy"), default="soft")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", type=int, default=0)
@@ -204,20 +217,37 @@ def main(argv=None):
                        device=dev)
     ws_v = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_VERIFY, B, K, R, d, V), dtype=torch.uint8,
                        device=dev)
+    greedy = args.mode == "greedy"
+    am = torch.empty((B, K, R), dtype=torch.int32, device=dev)
+    ws_h = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_HEAD, B, K, R, d, V), dtype=torch.uint8,
+                       device=dev)
+    ws_g = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_VERIFY_GREEDY, B, K, R, d, V),
+                       dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     def step(t, ev=None):
         if ev is not None:
             ev[0].record(stream)
-        D.dbl_head_logprobs(h, w, tls, lmass, lse)
+        if greedy:
+            D.dbl_head_logprobs(h, w, tls, lmass, lse, argmax=am, ws=ws_h)
+        else:
+            D.dbl_head_logprobs(h, w, tls, lmass, lse)
         if ev is not None:
             ev[1].record(stream)
-        D.dbl_sample_block(tls, lmass, lse, ell, z_temp=wl.z_temp, seed=wl.philox_seed, step=t,
-                           z_out=z, x_out=x, ws=ws_s)
+        if greedy:
+            D.dbl_sample_greedy(am, ell, z_temp=wl.z_temp, seed=wl.philox_seed, step=t, V=V,
+                                z_out=z, x_out=x)
+        else:
+            D.dbl_sample_block(tls, lmass, lse, ell, z_temp=wl.z_temp, seed=wl.philox_seed,
+                               step=t, z_out=z, x_out=x, ws=ws_s)
         if ev is not None:
             ev[2].record(stream)
-        D.dbl_verify_block(tls, lmass, lse, ell, x, logp, z_temp=wl.z_temp, seed=wl.philox_seed,
-                           step=t, out=vout, ws=ws_v)
+        if greedy:
+            D.dbl_verify_greedy(am, ell, x, logp, z_temp=wl.z_temp, seed=wl.philox_seed, step=t,
+                                out=vout, ws=ws_g)
+        else:
+            D.dbl_verify_block(tls, lmass, lse, ell, x, logp, z_temp=wl.z_temp,
+                               seed=wl.philox_seed, step=t, out=vout, ws=ws_v)
         if ev is not None:
             ev[3].record(stream)
 
@@ -244,8 +274,11 @@ def main(argv=None):
     M = B * K * R
     head_flop = 2.0 * M * d * V
     head_tflops = head_flop / (head_ms * 1e-3) / 1e12
-    verify_bytes = B * K * (R + 1) * V * 4.0
-    sample_bytes = B * K * V * 4.0
+    # Algorithmic bytes: soft verify streams R branch rows + the target row per position; the
+    # soft draw one branch row per position. Greedy verify streams one target row per block
+    # (the first rejected position or the bonus row); the greedy draw reads no vocabulary row.
+    verify_bytes = B * V * 4.0 if greedy else B * K * (R + 1) * V * 4.0
+    sample_bytes = 0.0 if greedy else B * K * V * 4.0
     traffic = _traffic(args.workload)
 
     out = {
@@ -264,7 +297,7 @@ def main(argv=None):
         "config": {"workload": args.workload, "B": B, "K": K, "R": R, "d": d, "V": V,
                    "global_batch": B, "positions_per_step": B * K,
                    "target_temperature": wl.temperature, "z_temp": wl.z_temp,
-                   "parallelism": "single GPU"},
+                   "mode": args.mode, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": head_tflops, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": head_tflops / PEAK_BF16_TFLOPS,
                      "traffic": traffic,
@@ -278,7 +311,7 @@ def main(argv=None):
         "wall_s_timed": wall,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = _cpu_baseline(wl, h, w, ell, logp, args.cpu_budget)
+        out["cpu_baseline"] = _cpu_baseline(wl, h, w, ell, logp, args.cpu_budget, args.mode)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -188,3 +188,52 @@ def test_stress_workload_1000_step_loop():
     assert not np.array_equal(rec[0][1], rec[1][1])
     print(f"[fullsize] stress mean accepted per block-step "
           f"{(tot_acc.sum() / (B * steps)).item():.4f}", flush=True)
+
+
+def test_greedy_qwen3_8b_full_shape():
+    """Greedy-branch step at the Qwen3-8B shape in the benchmark's configuration: the head's
+    argmax on sampled rows against the oracle's binary64 argmax (certified near-ties only), then
+    the greedy draw and verification for every block against the oracle fed the same branch
+    tokens, at two target temperatures."""
+    from oracle import greedy as GR
+    from paper_2608_05448_amd import dblast as D
+    wl = synth.WORKLOADS["qwen3_8b"]
+    print(f"[fullsize] greedy qwen3_8b B={wl.B} K={wl.K} R={wl.R}", flush=True)
+    h = synth.make_h(wl, "cuda")
+    w = synth.make_w(wl, "cuda")
+    ell = synth.make_ell(wl, "cuda")
+    tls, lmass, lse, am = D.dbl_head_logprobs(h, w, argmax=True)
+    t2, l2, s2 = D.dbl_head_logprobs(h, w)
+    torch.cuda.synchronize()
+    assert torch.equal(tls, t2) and torch.equal(lmass, l2) and torch.equal(lse, s2)
+    xhat = am.cpu().numpy()
+    w_np = np32(w)
+    ties = 0
+    for b in (0, 7, 15):
+        logits = OH.head_logits(np32(h[b]).reshape(wl.K * wl.R, wl.d), w_np)
+        want = GR.branch_tokens(logits).reshape(wl.K, wl.R)
+        for k, z in zip(*np.nonzero(xhat[b] != want)):
+            row = logits[k * wl.R + z]
+            assert abs(row[xhat[b, k, z]] - row[want[k, z]]) <= 2e-4
+            ties += 1
+    print(f"[fullsize] greedy argmax certified near-ties {ties}", flush=True)
+    ell_np = ell.cpu().numpy()
+    seq = np.arange(wl.B)
+    z, x = D.dbl_sample_greedy(am, ell, z_temp=wl.z_temp, seed=wl.philox_seed, step=3, V=wl.V)
+    z_o, x_o = GR.sample_blocks_greedy(xhat, ell_np, wl.z_temp, wl.philox_seed, 3, seq)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(z.cpu().numpy(), z_o)
+    np.testing.assert_array_equal(x.cpu().numpy(), x_o)
+    for T in (0.0, 1.0):
+        logp = synth.make_logp(wl, rows=wl.K + 1, device="cuda", temperature=T)
+        out = D.dbl_verify_greedy(am, ell, x, logp, z_temp=wl.z_temp, seed=wl.philox_seed,
+                                  step=3)
+        torch.cuda.synchronize()
+        ref = GR.verify_blocks_greedy(xhat, ell_np, wl.z_temp, x_o, logp.cpu().numpy(),
+                                      wl.philox_seed, 3, seq)
+        np.testing.assert_array_equal(out["n_accept"].cpu().numpy(), ref["n_accept"])
+        np.testing.assert_array_equal(out["next_token"].cpu().numpy(), ref["next_token"])
+        assert _rel(out["accept_mass"].cpu().numpy(), ref["beta"]) < 1e-4
+        assert _rel(out["exp_len"].cpu().numpy(), ref["E"]) < 1e-4
+        print(f"[fullsize] greedy T={T}: mean n_accept {out['n_accept'].float().mean().item():.3f}",
+              flush=True)
