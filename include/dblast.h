@@ -17,6 +17,7 @@
  *   dbl_sample_block    category and token draw of one block per sequence
  *   dbl_verify_block    sequential accept test, residual or bonus draw, acceptance mass
  *   dbl_expected_len    acceptance mass and expected accepted length along a given trajectory
+ *   dbl_acceptance_objective  the training surrogate's forward quantities and the block NLL
  *
  * and the same three steps for the greedy-branch proposal that the paper's reported
  * experiments use (appendix "Greedy-Branch Proposal"): dbl_sample_greedy, dbl_verify_greedy,
@@ -257,6 +258,34 @@ dbl_status dbl_expected_len_greedy(dbl_shape shape, const int32_t* x_hat,
                                    const float* prior_logits, float z_temp, const int32_t* x,
                                    const float* logp, float* beta, float* exp_len, void* ws,
                                    size_t ws_bytes, void* stream);
+
+/*
+ * dbl_acceptance_objective - forward quantities of the acceptance-oriented training surrogate
+ * (Sec. "Acceptance-Oriented Training") along target trajectories x* (for example the target's
+ * own samples), for the dependent proposal with prior q_{Z_T} = softmax(l / Z_T):
+ *   log q(x*_{1:l}) = log sum_z q_{Z_T}(z) prod_{j<=l} q_j(x*_j | z)      (Eq. cp-drafter)
+ *   log_r[b, l-1]   = log q(x*_{1:l}) - sum_{j<=l} log p_j(x*_j)  (Eq. acceptance-length-objective)
+ *   A_j             = min(1, p_j(x*_j) / q(x*_j | x*_<j)),  q(x_j | x_<j) = q(x_{1:j}) / q(x_{1:j-1})
+ *   S[b, l-1]       = sum_{i<=l} prod_{j<=i} A_j
+ *   ell_tau[b]      = min({l : r_l < tau} U {K}), 1-based
+ *   J[b]            = sum_{l=1}^{ell_tau} (log r_l + log S_l)            (Eq. subblock-objective;
+ *                     the training loss is minus its mean, Eq. training-loss)
+ *   nll[b]          = -log q(x*_{1:K})                                  (Eq. dependent-nll)
+ * Arithmetic is binary64 on the binary32 inputs (lq = fl32(tls + fl32(lmass - lse)) as
+ * everywhere); outputs are binary32.
+ *   tls, lmass, lse, prior_logits, z_temp   as dbl_expected_len
+ *   x       [B, K] int32 trajectory (ids outside [0, V) have probability 0 on both sides)
+ *   logp    [B, K, V] fp32 target log-probabilities of the filter that generated x
+ *   tau     truncation threshold, finite and > 0 (the paper uses 0.1)
+ *   log_r, S  out [B, K] fp32 or NULL;  ell_tau out [B] int32;  J, nll out [B] fp32
+ * No workspace. Errors: DBL_EINVAL for null pointers, z_temp < 0 or NaN, tau <= 0 or not
+ * finite; DBL_ESHAPE.
+ */
+dbl_status dbl_acceptance_objective(dbl_shape shape, const float* tls, const float* lmass,
+                                    const float* lse, const float* prior_logits, float z_temp,
+                                    const int32_t* x, const float* logp, float tau, float* log_r,
+                                    float* S, int32_t* ell_tau, float* J, float* nll,
+                                    void* stream);
 
 #ifdef __cplusplus
 }

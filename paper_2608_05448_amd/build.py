@@ -26,6 +26,7 @@ SOURCES = {
     "sample.hip": ["-ffp-contract=off"],
     "verify.hip": ["-ffp-contract=off"],
     "greedy.hip": ["-ffp-contract=off"],
+    "objective.hip": [],
 }
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -361,4 +361,28 @@ dbl_status dbl_expected_len_greedy(dbl_shape s, const int32_t* x_hat,
                     "greedy expected_len launch");
 }
 
+dbl_status dbl_acceptance_objective(dbl_shape s, const float* tls, const float* lmass,
+                                    const float* lse, const float* prior_logits, float z_temp,
+                                    const int32_t* x, const float* logp, float tau, float* log_r,
+                                    float* S, int32_t* ell_tau, float* J, float* nll,
+                                    void* stream) {
+  if (dbl_status st = check_block_inputs(s, tls, lmass, lse, prior_logits, z_temp)) return st;
+  if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
+  if (!ell_tau || !J || !nll) return fail(DBL_EINVAL, "NULL output pointer");
+  if (!(tau > 0.0f) || isinf(tau)) return fail(DBL_EINVAL, "tau must be finite and > 0");
+  if (s.B == 0) return ok();
+  dbl::ObjectiveArgs a{};
+  a.blk = block_args(s, tls, lmass, lse, prior_logits, z_temp, 0, 0, 0);
+  a.x = x;
+  a.logp = logp;
+  a.tau = tau;
+  a.log_r = log_r;
+  a.S = S;
+  a.ell_tau = ell_tau;
+  a.J = J;
+  a.nll = nll;
+  return hip_status(dbl::launch_objective(a, static_cast<hipStream_t>(stream)),
+                    "objective launch");
+}
+
 }  // extern "C"

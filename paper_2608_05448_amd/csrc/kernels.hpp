@@ -81,6 +81,19 @@ struct GreedyArgs {
   uint64_t* p_tiles;    // workspace [B, nT]
 };
 
+// Training-objective forward along target trajectories.
+struct ObjectiveArgs {
+  BlockArgs blk;
+  const int32_t* x;     // [B, K] target trajectory
+  const float* logp;    // [B, K, V]
+  float tau;
+  float* log_r;         // [B, K] or null
+  float* S;             // [B, K] or null
+  int32_t* ell_tau;     // [B]
+  float* J;             // [B]
+  float* nll;           // [B]
+};
+
 inline int n_chunks(int nT) { return (nT + kTilesPerChunk - 1) / kTilesPerChunk; }
 
 hipError_t launch_head(const HeadArgs& a, hipStream_t stream);
@@ -88,5 +101,6 @@ hipError_t launch_sample(const SampleArgs& a, hipStream_t stream);
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
 hipError_t launch_sample_greedy(const GreedyArgs& a, hipStream_t stream);
 hipError_t launch_verify_greedy(const GreedyArgs& a, hipStream_t stream);
+hipError_t launch_objective(const ObjectiveArgs& a, hipStream_t stream);
 
 }  // namespace dbl

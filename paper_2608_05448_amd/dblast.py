@@ -57,6 +57,8 @@ _SIGS = {
     "dbl_verify_greedy": (ctypes.c_int, [Shape, _P, _P, _F, _P, _P, _I64, _U64, _U64, _I64, _P,
                                          _P, _P, _P, _P, _P, _SZ, _P]),
     "dbl_expected_len_greedy": (ctypes.c_int, [Shape, _P, _P, _F, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dbl_acceptance_objective": (ctypes.c_int, [Shape, _P, _P, _P, _P, _F, _P, _P, _F, _P, _P,
+                                                _P, _P, _P, _P]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -311,3 +313,28 @@ def dbl_expected_len_greedy(x_hat, prior_logits, x, logp, z_temp=1.0, want_beta=
                                           _ptr(x), _ptr(logp), _ptr(beta), _ptr(exp_len),
                                           _ptr(ws), nws, _stream(dev)))
     return beta, exp_len
+
+
+def dbl_acceptance_objective(tls, lmass, lse, prior_logits, x, logp, z_temp=1.0, tau=0.1,
+                             want_terms=True, out=None):
+    """Training-surrogate forward along target trajectories x [B, K] with target log-probs
+    logp [B, K, V]: returns a dict with ell_tau [B] int32, J [B], nll [B] and, with
+    ``want_terms``, log_r [B, K] and S [B, K] (fp32)."""
+    shape = _block_shape(tls, lmass, lse, prior_logits)
+    dev = tls.device
+    B, K, V = shape.B, shape.K, shape.V
+    _need(x, "x", torch.int32, (B, K))
+    _need(logp, "logp", torch.float32, (B, K, V))
+    o = {} if out is None else dict(out)
+    o.setdefault("ell_tau", torch.empty(B, dtype=torch.int32, device=dev))
+    o.setdefault("J", torch.empty(B, dtype=torch.float32, device=dev))
+    o.setdefault("nll", torch.empty(B, dtype=torch.float32, device=dev))
+    if want_terms:
+        o.setdefault("log_r", torch.empty((B, K), dtype=torch.float32, device=dev))
+        o.setdefault("S", torch.empty((B, K), dtype=torch.float32, device=dev))
+    _check(load().dbl_acceptance_objective(shape, _ptr(tls), _ptr(lmass), _ptr(lse),
+                                           _ptr(prior_logits), float(z_temp), _ptr(x),
+                                           _ptr(logp), float(tau), _ptr(o.get("log_r")),
+                                           _ptr(o.get("S")), _ptr(o["ell_tau"]), _ptr(o["J"]),
+                                           _ptr(o["nll"]), _stream(dev)))
+    return o

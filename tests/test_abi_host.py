@@ -186,3 +186,20 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
             D.load(str(tmp_path / "missing.so"))
     finally:
         D._lib = saved
+
+
+def test_objective_validation(lib):
+    S = D.Shape
+    p = _fake(10)
+    null = ctypes.c_void_p(None)
+    shape = S(2, 4, 3, 0, 300)
+    for tau in (0.0, -1.0, float("inf"), float("nan")):
+        assert lib.dbl_acceptance_objective(shape, p[0], p[1], p[2], p[3], 1.0, p[4], p[5], tau,
+                                            null, null, p[6], p[7], p[8], null) == D.DBL_EINVAL
+    assert lib.dbl_acceptance_objective(shape, p[0], p[1], p[2], p[3], -1.0, p[4], p[5], 0.1,
+                                        null, null, p[6], p[7], p[8], null) == D.DBL_EINVAL
+    assert lib.dbl_acceptance_objective(shape, p[0], p[1], p[2], p[3], 1.0, p[4], p[5], 0.1,
+                                        null, null, null, p[7], p[8], null) == D.DBL_EINVAL
+    assert lib.dbl_acceptance_objective(S(0, 4, 3, 0, 300), p[0], p[1], p[2], p[3], 1.0, p[4],
+                                        p[5], 0.1, null, null, p[6], p[7], p[8],
+                                        null) == D.DBL_OK

@@ -97,8 +97,9 @@ def test_e2e_qwen3_8b_sampled_blocks_all_temperatures():
 
 
 def test_objective_workload_chunked_expected_length():
-    """2048 blocks x K=16 x R=16 at d=4096: chunks of 128 blocks through the head and the
-    expected-length reduction along target trajectories."""
+    """2048 blocks x K=16 x R=16 at d=4096: chunks of 128 blocks through the head, the
+    expected-length reduction and the training-objective forward along target trajectories."""
+    from oracle import objective as OB
     from paper_2608_05448_amd import dblast as D
     wl = synth.WORKLOADS["objective"]
     chunk = 128
@@ -107,6 +108,9 @@ def test_objective_workload_chunked_expected_length():
     ell = synth.make_ell(wl, "cuda")
     beta_all = torch.empty((wl.B, wl.K), dtype=torch.float32, device="cuda")
     e_all = torch.empty(wl.B, dtype=torch.float32, device="cuda")
+    j_all = torch.empty(wl.B, dtype=torch.float32, device="cuda")
+    lt_all = torch.empty(wl.B, dtype=torch.int32, device="cuda")
+    nll_all = torch.empty(wl.B, dtype=torch.float32, device="cuda")
     check = {5: None, 1500: None, 2047: None}
     for c0 in range(0, wl.B, chunk):
         blocks = range(c0, c0 + chunk)
@@ -118,6 +122,11 @@ def test_objective_workload_chunked_expected_length():
                                      z_temp=wl.z_temp)
         beta_all[c0:c0 + chunk] = beta
         e_all[c0:c0 + chunk] = e
+        obj = D.dbl_acceptance_objective(tls, lmass, lse, ell[c0:c0 + chunk].contiguous(), xs,
+                                         logp, z_temp=wl.z_temp, tau=0.1, want_terms=False)
+        j_all[c0:c0 + chunk] = obj["J"]
+        lt_all[c0:c0 + chunk] = obj["ell_tau"]
+        nll_all[c0:c0 + chunk] = obj["nll"]
         for b in check:
             if c0 <= b < c0 + chunk:
                 i = b - c0
@@ -134,8 +143,18 @@ def test_objective_workload_chunked_expected_length():
                                              lp[None])
         assert _rel(beta_all[b].cpu().numpy(), beta_o[0]) < 1e-4
         assert _rel([e_all[b].item()], e_o) < 1e-4
+        ob = OB.acceptance_objective(lq[None], ell_np[b:b + 1], wl.z_temp, xs[None], lp[None],
+                                     tau=0.1)
+        assert abs(nll_all[b].item() - ob["nll"][0]) < 1e-4 * max(1.0, abs(ob["nll"][0]))
+        if lt_all[b].item() == ob["ell_tau"][0]:
+            assert abs(j_all[b].item() - ob["J"][0]) < 1e-4 * max(1.0, abs(ob["J"][0]))
+        else:   # end to end the two heads differ by ~1e-6 per log-prob: a near-tie only
+            l = min(lt_all[b].item(), int(ob["ell_tau"][0]))
+            assert abs(ob["log_r"][0, l - 1] - np.log(0.1)) < 1e-3
         print(f"[fullsize] objective block {b}: E={e_o[0]:.6f} ok", flush=True)
-    print(f"[fullsize] objective mean E over {wl.B} blocks: {e_all.mean().item():.5f}", flush=True)
+    print(f"[fullsize] objective mean E over {wl.B} blocks: {e_all.mean().item():.5f}; mean "
+          f"l_tau {lt_all.float().mean().item():.2f}, mean J {j_all.mean().item():.3f}, mean NLL "
+          f"{nll_all.mean().item():.3f}", flush=True)
 
 
 def test_stress_workload_1000_step_loop():
