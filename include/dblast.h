@@ -18,6 +18,7 @@
  *   dbl_verify_block    sequential accept test, residual or bonus draw, acceptance mass
  *   dbl_expected_len    acceptance mass and expected accepted length along a given trajectory
  *   dbl_acceptance_objective  the training surrogate's forward quantities and the block NLL
+ *   dbl_expand_branches / dbl_prior_head  the head's inputs: branch states and category logits
  *
  * and the same three steps for the greedy-branch proposal that the paper's reported
  * experiments use (appendix "Greedy-Branch Proposal"): dbl_sample_greedy, dbl_verify_greedy,
@@ -54,7 +55,8 @@
  * Conventions for every call:
  *  - Ownership: every data pointer is a device pointer owned by the caller; the library never
  *    allocates device memory. Scratch space is a caller-provided device workspace of at least
- *    dbl_workspace_bytes(op, shape) bytes, 256-byte aligned.
+ *    dbl_workspace_bytes(op, shape) bytes, 256-byte aligned. Array arguments must be 16-byte
+ *    aligned (vector loads and stores; any allocator's base pointer is).
  *  - Streams: work is enqueued on `stream` (a hipStream_t; NULL is the default stream) and the
  *    call returns without waiting. Outputs are valid once the stream reaches that point.
  *  - Errors: a non-zero dbl_status is returned before anything is launched when an argument is
@@ -286,6 +288,35 @@ dbl_status dbl_acceptance_objective(dbl_shape shape, const float* tls, const flo
                                     const int32_t* x, const float* logp, float tau, float* log_r,
                                     float* S, int32_t* ell_tau, float* J, float* nll,
                                     void* stream);
+
+/*
+ * dbl_expand_branches - the category hidden expander (Sec. "Architecture"): every trunk state
+ * h_k of a block position becomes R branch states
+ *     h_{k,z} = h_k + g_z(h_k),   g_z(h) = W_z h + c_z,
+ * with the expander a single linear layer H -> R*H (the added parameters of Table 4 besides the
+ * prior head). One bf16 MFMA GEMM of the B*K trunk rows against W, fp32 accumulation; the bias
+ * and the residual are added in fp32 and the result is rounded once to bf16.
+ *   shape   B, K, R, d used (V unused); d % 32 == 0
+ *   h       [B, K, d] bf16 trunk states
+ *   W       [R*d, d] bf16 (nn.Linear layout; output feature z*d + j is component j of g_z)
+ *   c       [R*d] bf16 bias
+ *   h_out   out [B, K, R, d] bf16: the dbl_head_logprobs input h
+ * No workspace. Errors: DBL_EINVAL for null pointers; DBL_ESHAPE for d % 32 != 0 or a dimension
+ * out of range.
+ */
+dbl_status dbl_expand_branches(dbl_shape shape, const void* h, const void* W, const void* c,
+                               void* h_out, void* stream);
+
+/*
+ * dbl_prior_head - the category-prior head (Sec. "Architecture"): l[b, z] = U[z] . h_anchor[b]
+ * + e[z], the category logits l_z(y) that dbl_sample_block / dbl_verify_block take as
+ * prior_logits. fp32 accumulation of bf16 inputs.
+ *   shape     B, R, d used;  h_anchor [B, d] bf16 block-anchor states;  U [R, d] bf16;
+ *   e         [R] bf16;  prior_logits out [B, R] fp32
+ * No workspace. Errors: DBL_EINVAL for null pointers; DBL_ESHAPE.
+ */
+dbl_status dbl_prior_head(dbl_shape shape, const void* h_anchor, const void* U, const void* e,
+                          float* prior_logits, void* stream);
 
 #ifdef __cplusplus
 }

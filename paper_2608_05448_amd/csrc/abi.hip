@@ -385,4 +385,43 @@ dbl_status dbl_acceptance_objective(dbl_shape s, const float* tls, const float* 
                     "objective launch");
 }
 
+dbl_status dbl_expand_branches(dbl_shape s, const void* h, const void* W, const void* c,
+                               void* h_out, void* stream) {
+  if (s.B < 0 || s.K < 1 || s.R < 1 || s.R > dbl::kMaxR)
+    return fail(DBL_ESHAPE, "need B >= 0, K >= 1 and 1 <= R <= 64");
+  if (s.d < 32 || s.d % 32 != 0 || s.d > (int64_t(1) << 20))
+    return fail(DBL_ESHAPE, "expander needs d % 32 == 0 and 32 <= d <= 2^20");
+  if (static_cast<double>(s.B) * s.K * s.R * s.d >= 4.0e18)
+    return fail(DBL_ESHAPE, "B*K*R*d too large");
+  if (!h || !W || !c || !h_out) return fail(DBL_EINVAL, "NULL pointer");
+  if (s.B == 0) return ok();
+  dbl::ExpandArgs a;
+  a.M = s.B * s.K;
+  a.R = s.R;
+  a.d = static_cast<int>(s.d);
+  a.h = h;
+  a.W = W;
+  a.c = c;
+  a.out = h_out;
+  return hip_status(dbl::launch_expand(a, static_cast<hipStream_t>(stream)), "expander launch");
+}
+
+dbl_status dbl_prior_head(dbl_shape s, const void* h_anchor, const void* U, const void* e,
+                          float* prior_logits, void* stream) {
+  if (s.B < 0 || s.R < 1 || s.R > dbl::kMaxR || s.d < 1 || s.d > (int64_t(1) << 30))
+    return fail(DBL_ESHAPE, "need B >= 0, 1 <= R <= 64 and 1 <= d <= 2^30");
+  if (!h_anchor || !U || !e || !prior_logits) return fail(DBL_EINVAL, "NULL pointer");
+  if (s.B == 0) return ok();
+  dbl::PriorHeadArgs a;
+  a.B = s.B;
+  a.R = static_cast<int>(s.R);
+  a.d = static_cast<int>(s.d);
+  a.h_anchor = h_anchor;
+  a.U = U;
+  a.e = e;
+  a.ell = prior_logits;
+  return hip_status(dbl::launch_prior_head(a, static_cast<hipStream_t>(stream)),
+                    "prior head launch");
+}
+
 }  // extern "C"

@@ -413,11 +413,67 @@ __device__ __forceinline__ void wait_vmcnt() {
 #endif
 using DCfg = DmaCfg<DBL_HEAD_BK, DBL_HEAD_STAGES, DBL_HEAD_BM, DBL_HEAD_WM>;
 
-template <class C, bool ARG>
+// What the direct-to-LDS GEMM does with its accumulators (rows of w on the MFMA rows, rows of h
+// on the columns): the head's tile log-softmax (with or without the argmax keys), or the
+// category expander's branch states.
+enum EpiKind : int { kEpiLogSoftmax = 0, kEpiLogSoftmaxArgmax = 1, kEpiExpand = 2 };
+
+struct EpiArgs {
+  float* tls;            // head: [M, V]
+  float* lmass;          // head: [M, nT]
+  uint64_t* amax;        // head: [M] argmax keys (argmax epilogue)
+  int nT, vec4;
+  __bf16* out;           // expander: [M, V] branch states, V = R * d
+  const __bf16* bias;    // expander: [V]
+  const __bf16* hres;    // expander: [M, d] trunk states (the residual)
+  int dres;              // expander: d
+};
+
+// Expander epilogue: out[m, v] = bf16(h[m, v mod d] + (acc + c[v])), i.e. h_{k,z} = h_k + g_z(h_k)
+// with g_z(h) = W_z h + c_z evaluated in fp32 and rounded once. Lane l holds row
+// m0w + 32 cb + l % 32 and, in registers 4g..4g+3 of row block rb, the four consecutive features
+// v0w + 32 rb + 8 g + 4 (l / 32) + {0..3}, which are stored as one 8-byte write.
+template <int NRB, int NCB>
+__device__ __forceinline__ void expand_store(f32x16 (&acc)[NRB][NCB], const EpiArgs& e,
+                                             int64_t M, int64_t V, int64_t v0w, int64_t m0w,
+                                             int lane) {
+  const int half = lane >> 5;
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    const int64_t m = m0w + cb * 32 + (lane & 31);
+    if (m >= M) continue;
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int64_t v = v0w + 32 * rb + 8 * g + 4 * half;
+        if (v >= V) continue;
+        const int64_t j = v % e.dres;
+        const __bf16* hr = e.hres + m * e.dres + j;
+        __bf16* o = e.out + m * V + v;
+        if (v + 3 < V) {
+          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          const bf16x4 c4 = *reinterpret_cast<const bf16x4*>(e.bias + v);
+          const bf16x4 h4 = *reinterpret_cast<const bf16x4*>(hr);
+          bf16x4 y;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            y[q] = static_cast<__bf16>(static_cast<float>(h4[q]) +
+                                       (acc[rb][cb][4 * g + q] + static_cast<float>(c4[q])));
+          *reinterpret_cast<bf16x4*>(o) = y;
+        } else {
+          for (int q = 0; q < 4 && v + q < V; ++q)
+            o[q] = static_cast<__bf16>(static_cast<float>(hr[q]) +
+                                       (acc[rb][cb][4 * g + q] + static_cast<float>(e.bias[v + q])));
+        }
+      }
+  }
+}
+
+template <class C, int EPI>
 __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel(
-    const __bf16* __restrict__ h, const __bf16* __restrict__ w, float* __restrict__ tls,
-    float* __restrict__ lmass, uint64_t* __restrict__ amax, int64_t M, int64_t V, int d, int nT,
-    int n_mtiles, int vec4) {
+    const __bf16* __restrict__ h, const __bf16* __restrict__ w, const EpiArgs ea, int64_t M,
+    int64_t V, int d, int n_mtiles) {
   constexpr int TA = C::TBA, TB = C::TBB;
   __shared__ __attribute__((aligned(1024))) char sA0[TA], sB0[TB], sA1[TA], sB1[TB];
   __shared__ __attribute__((aligned(1024))) char sA2[C::S > 2 ? TA : 16], sB2[C::S > 2 ? TB : 16];
@@ -594,8 +650,11 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
 
   const int64_t v0w = v0 + wv * kVTile;
   if (v0w >= V) return;
-  tile_logsoftmax_store<C::NRB, C::NCB, ARG>(acc, tls, lmass, amax, M, V, nT, v0w,
-                                             m0 + wm * C::TM, lane, vec4);
+  if constexpr (EPI == kEpiExpand)
+    expand_store<C::NRB, C::NCB>(acc, ea, M, V, v0w, m0 + wm * C::TM, lane);
+  else
+    tile_logsoftmax_store<C::NRB, C::NCB, EPI == kEpiLogSoftmaxArgmax>(
+        acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w, m0 + wm * C::TM, lane, ea.vec4);
 }
 
 // fp32 path: workgroup (vocabulary tile t, 4 branch rows); thread j owns id 128 t + j.
@@ -739,12 +798,18 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
       const int64_t dwg = ((a.V + DCfg::BV - 1) / DCfg::BV) * dm;
       if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
       const dim3 grid(static_cast<unsigned>(dwg)), block(DCfg::kThreads);
+      EpiArgs ea{};
+      ea.tls = a.tls;
+      ea.lmass = a.lmass;
+      ea.amax = amax;
+      ea.nT = nT;
+      ea.vec4 = vec4;
       if (amax)
-        hipLaunchKernelGGL((head_bf16_dma_kernel<DCfg, true>), grid, block, 0, stream, h, w,
-                           a.tls, a.lmass, amax, a.M, a.V, a.d, nT, dm, vec4);
+        hipLaunchKernelGGL((head_bf16_dma_kernel<DCfg, kEpiLogSoftmaxArgmax>), grid, block, 0,
+                           stream, h, w, ea, a.M, a.V, a.d, dm);
       else
-        hipLaunchKernelGGL((head_bf16_dma_kernel<DCfg, false>), grid, block, 0, stream, h, w,
-                           a.tls, a.lmass, amax, a.M, a.V, a.d, nT, dm, vec4);
+        hipLaunchKernelGGL((head_bf16_dma_kernel<DCfg, kEpiLogSoftmax>), grid, block, 0, stream,
+                           h, w, ea, a.M, a.V, a.d, dm);
     } else {
       const dim3 grid(static_cast<unsigned>(nwg)), block(Cfg::kThreads);
       if (amax)
@@ -766,6 +831,56 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
   const int64_t lse_blocks = (a.M + 3) / 4;
   hipLaunchKernelGGL(lse_finalize_kernel, dim3(static_cast<unsigned>(lse_blocks)), dim3(256), 0,
                      stream, a.lmass, a.lse, amax, amax ? a.argmax : nullptr, a.M, nT);
+  return hipGetLastError();
+}
+
+namespace {
+
+// Category-prior head: l[b, z] = sum_j U[z, j] h_anchor[b, j] + e[z] in fp32 accumulation.
+// One workgroup per block; every category's dot product is a workgroup reduction.
+__global__ __launch_bounds__(256) void prior_head_kernel(const __bf16* __restrict__ ha,
+                                                         const __bf16* __restrict__ U,
+                                                         const __bf16* __restrict__ e,
+                                                         float* __restrict__ ell, int R, int d) {
+  __shared__ float red[4];
+  const int64_t b = blockIdx.x;
+  const __bf16* hb = ha + b * d;
+  for (int z = 0; z < R; ++z) {
+    const __bf16* u = U + static_cast<int64_t>(z) * d;
+    float s = 0.0f;
+    for (int j = threadIdx.x; j < d; j += 256)
+      s = fmaf(static_cast<float>(u[j]), static_cast<float>(hb[j]), s);
+    s = wave_sum(s);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) ell[b * R + z] = ((red[0] + red[1]) + (red[2] + red[3])) + static_cast<float>(e[z]);
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {
+  const int64_t N = a.R * a.d;
+  const int dm = static_cast<int>((a.M + DCfg::BM - 1) / DCfg::BM);
+  const int64_t dwg = ((N + DCfg::BV - 1) / DCfg::BV) * dm;
+  if (dwg > 0x7fffffff || a.d % DCfg::BK != 0) return hipErrorInvalidConfiguration;
+  EpiArgs ea{};
+  ea.out = static_cast<__bf16*>(a.out);
+  ea.bias = static_cast<const __bf16*>(a.c);
+  ea.hres = static_cast<const __bf16*>(a.h);
+  ea.dres = a.d;
+  hipLaunchKernelGGL((head_bf16_dma_kernel<DCfg, kEpiExpand>), dim3(static_cast<unsigned>(dwg)),
+                     dim3(DCfg::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
+                     static_cast<const __bf16*>(a.W), ea, a.M, N, a.d, dm);
+  return hipGetLastError();
+}
+
+hipError_t launch_prior_head(const PriorHeadArgs& a, hipStream_t stream) {
+  if (a.B > 0x7fffffff) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(prior_head_kernel, dim3(static_cast<unsigned>(a.B)), dim3(256), 0, stream,
+                     static_cast<const __bf16*>(a.h_anchor), static_cast<const __bf16*>(a.U),
+                     static_cast<const __bf16*>(a.e), a.ell, a.R, a.d);
   return hipGetLastError();
 }
 

@@ -94,6 +94,26 @@ struct ObjectiveArgs {
   float* nll;           // [B]
 };
 
+// Category hidden expander (bf16): out[m, z*d + j] = h[m, j] + (W h[m])[z*d + j] + c[z*d + j].
+struct ExpandArgs {
+  int64_t M, R;
+  int d;
+  const void* h;   // [M, d]
+  const void* W;   // [R*d, d]
+  const void* c;   // [R*d]
+  void* out;       // [M, R*d]
+};
+
+// Category-prior head (bf16 inputs, fp32 logits): ell[b, z] = U[z] . h_anchor[b] + e[z].
+struct PriorHeadArgs {
+  int64_t B;
+  int R, d;
+  const void* h_anchor;  // [B, d]
+  const void* U;         // [R, d]
+  const void* e;         // [R]
+  float* ell;            // [B, R]
+};
+
 inline int n_chunks(int nT) { return (nT + kTilesPerChunk - 1) / kTilesPerChunk; }
 
 hipError_t launch_head(const HeadArgs& a, hipStream_t stream);
@@ -102,5 +122,7 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream);
 hipError_t launch_sample_greedy(const GreedyArgs& a, hipStream_t stream);
 hipError_t launch_verify_greedy(const GreedyArgs& a, hipStream_t stream);
 hipError_t launch_objective(const ObjectiveArgs& a, hipStream_t stream);
+hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
+hipError_t launch_prior_head(const PriorHeadArgs& a, hipStream_t stream);
 
 }  // namespace dbl

@@ -59,6 +59,8 @@ _SIGS = {
     "dbl_expected_len_greedy": (ctypes.c_int, [Shape, _P, _P, _F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dbl_acceptance_objective": (ctypes.c_int, [Shape, _P, _P, _P, _P, _F, _P, _P, _F, _P, _P,
                                                 _P, _P, _P, _P]),
+    "dbl_expand_branches": (ctypes.c_int, [Shape, _P, _P, _P, _P, _P]),
+    "dbl_prior_head": (ctypes.c_int, [Shape, _P, _P, _P, _P, _P]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -338,3 +340,33 @@ def dbl_acceptance_objective(tls, lmass, lse, prior_logits, x, logp, z_temp=1.0,
                                            _ptr(o.get("S")), _ptr(o["ell_tau"]), _ptr(o["J"]),
                                            _ptr(o["nll"]), _stream(dev)))
     return o
+
+
+def dbl_expand_branches(h, W, c, R, out=None):
+    """Branch states h_{k,z} = h_k + W_z h_k + c_z: h [B, K, d] bf16, W [R*d, d], c [R*d] bf16.
+    Returns [B, K, R, d] bf16 (the head's input)."""
+    B, K, d = h.shape
+    _need(h, "h", torch.bfloat16)
+    _need(W, "W", torch.bfloat16, (R * d, d))
+    _need(c, "c", torch.bfloat16, (R * d,))
+    dev = h.device
+    out = torch.empty((B, K, R, d), dtype=torch.bfloat16, device=dev) if out is None else out
+    _need(out, "out", torch.bfloat16, (B, K, R, d))
+    _check(load().dbl_expand_branches(Shape(B, K, R, d, 1), _ptr(h), _ptr(W), _ptr(c), _ptr(out),
+                                      _stream(dev)))
+    return out
+
+
+def dbl_prior_head(h_anchor, U, e, out=None):
+    """Category logits l = U h_anchor + e: h_anchor [B, d], U [R, d], e [R] bf16 -> [B, R] fp32."""
+    B, d = h_anchor.shape
+    R = U.shape[0]
+    _need(h_anchor, "h_anchor", torch.bfloat16)
+    _need(U, "U", torch.bfloat16, (R, d))
+    _need(e, "e", torch.bfloat16, (R,))
+    dev = h_anchor.device
+    out = torch.empty((B, R), dtype=torch.float32, device=dev) if out is None else out
+    _need(out, "out", torch.float32, (B, R))
+    _check(load().dbl_prior_head(Shape(B, 1, R, d, 1), _ptr(h_anchor), _ptr(U), _ptr(e),
+                                 _ptr(out), _stream(dev)))
+    return out

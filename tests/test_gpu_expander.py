@@ -1,0 +1,117 @@
+"""GPU parity of dbl_expand_branches and dbl_prior_head against the oracle (Sec. "Architecture").
+
+The expander output is bf16: the GPU rounds its fp32 result once, the oracle rounds the exact
+binary64 value once. They agree except where the exact value lies within the fp32 error of a
+bf16 rounding midpoint; every element must lie within half a bf16 ulp plus that error of the
+exact value, and at least 99% must be identical. Prior logits are fp32 accumulations, compared
+against binary64 within the accumulation error bound.
+"""
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import expander as EX
+
+pytestmark = pytest.mark.gpu
+
+
+def _np(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+EXPAND_CASES = [
+    # name, B, K, R, d
+    ("small", 2, 4, 3, 64),
+    ("ragged-rows", 1, 7, 5, 96),
+    ("qwen3-4b-paper-R", 1, 16, 4, 2560),
+    ("qwen3-8b-R8", 16, 16, 8, 4096),
+    ("max-categories", 1, 3, 64, 64),
+]
+
+
+@pytest.mark.parametrize("case", EXPAND_CASES, ids=[c[0] for c in EXPAND_CASES])
+def test_expander_parity(case):
+    from paper_2608_05448_amd import dblast as D
+    name, B, K, R, d = case
+    print(f"[expander] {name} B={B} K={K} R={R} d={d}", flush=True)
+    h = synth.make_uniform_logits((B, K, d), 11).to(torch.bfloat16)
+    W = (synth.make_uniform_logits((R * d, d), 12) * (0.5 / d ** 0.5)).to(torch.bfloat16)
+    c = (synth.make_uniform_logits((R * d,), 13) * 0.1).to(torch.bfloat16)
+    hd, Wd, cd = h.cuda(), W.cuda(), c.cuda()
+    out = D.dbl_expand_branches(hd, Wd, cd, R)
+    torch.cuda.synchronize()
+    if B * K * R * d >= 1 << 22:   # time the benchmark-sized case
+        n = 10
+        t0 = time.perf_counter()
+        for _ in range(n):
+            D.dbl_expand_branches(hd, Wd, cd, R, out=out)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) / n * 1e3
+        print(f"[expander] {name}: {ms:.3f} ms, {2 * B * K * R * d * d / ms / 1e9:.1f} TFLOP/s",
+              flush=True)
+    got = _np(out)
+    hh, WW, cc = _np(h), _np(W), _np(c)
+    if B * K > 64:   # check a sample of rows at the large shape
+        rows = np.random.default_rng(0).choice(B * K, 48, replace=False)
+    else:
+        rows = np.arange(B * K)
+    exact = EX.expand_branches(hh.reshape(-1, d)[rows], WW, cc)          # [n, R, d]
+    g = got.reshape(B * K, R, d)[rows]
+    ulp = np.ldexp(1.0, np.frexp(exact)[1] - 8)
+    err_bound = 0.5 * ulp + 1e-5 * np.abs(exact) + 1e-6
+    assert np.all(np.abs(g - exact) <= err_bound)
+    same = np.mean(g == EX.bf16_round(exact))
+    assert same > 0.99, same
+
+
+def test_zero_expander_copies_the_trunk_state():
+    from paper_2608_05448_amd import dblast as D
+    B, K, R, d = 3, 5, 4, 128
+    h = synth.make_uniform_logits((B, K, d), 21).to(torch.bfloat16).cuda()
+    W = torch.zeros((R * d, d), dtype=torch.bfloat16, device="cuda")
+    c = torch.zeros(R * d, dtype=torch.bfloat16, device="cuda")
+    out = D.dbl_expand_branches(h, W, c, R)
+    torch.cuda.synchronize()
+    for z in range(R):
+        assert torch.equal(out[:, :, z], h)
+
+
+def test_expander_feeds_the_head():
+    """Expander -> head on the GPU against the oracle chain (rounded branch states -> binary64
+    head) within the bf16 head tolerance."""
+    from oracle import head as OH
+    from paper_2608_05448_amd import dblast as D
+    B, K, R, d, V = 1, 4, 3, 256, 3000
+    h = synth.make_uniform_logits((B, K, d), 31).to(torch.bfloat16)
+    W = (synth.make_uniform_logits((R * d, d), 32) * (0.5 / d ** 0.5)).to(torch.bfloat16)
+    c = (synth.make_uniform_logits((R * d,), 33) * 0.1).to(torch.bfloat16)
+    w = (synth.make_uniform_logits((V, d), 34) * (2.0 / d ** 0.5)).to(torch.bfloat16)
+    hb = D.dbl_expand_branches(h.cuda(), W.cuda(), c.cuda(), R)
+    tls, lmass, lse = D.dbl_head_logprobs(hb, w.cuda())
+    torch.cuda.synchronize()
+    branch = EX.expand_branches(_np(h), _np(W), _np(c), round_bf16=True).reshape(-1, d)
+    want = OH.head_logq(branch, _np(w))
+    from cases import flat_from_factored
+    got = flat_from_factored(tls.cpu().numpy(), lmass.cpu().numpy(), lse.cpu().numpy())
+    assert np.max(np.abs(got.reshape(-1, V) - want)) < 2e-3
+
+
+PRIOR_CASES = [("small", 3, 4, 64), ("paper-R", 16, 4, 4096), ("many", 300, 64, 2560)]
+
+
+@pytest.mark.parametrize("case", PRIOR_CASES, ids=[c[0] for c in PRIOR_CASES])
+def test_prior_head_parity(case):
+    from paper_2608_05448_amd import dblast as D
+    name, B, R, d = case
+    print(f"[prior head] {name} B={B} R={R} d={d}", flush=True)
+    ha = synth.make_uniform_logits((B, d), 41).to(torch.bfloat16)
+    U = (synth.make_uniform_logits((R, d), 42) * (1.0 / d ** 0.5)).to(torch.bfloat16)
+    e = synth.make_uniform_logits((R,), 43).to(torch.bfloat16)
+    ell = D.dbl_prior_head(ha.cuda(), U.cuda(), e.cuda())
+    torch.cuda.synchronize()
+    want = EX.prior_logits(_np(ha), _np(U), _np(e))
+    bound = 1e-5 * (np.abs(_np(ha)) @ np.abs(_np(U)).T + np.abs(_np(e))) + 1e-6
+    assert np.all(np.abs(ell.cpu().numpy() - want) <= bound)
