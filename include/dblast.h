@@ -19,6 +19,8 @@
  *   dbl_expected_len    acceptance mass and expected accepted length along a given trajectory
  *   dbl_acceptance_objective  the training surrogate's forward quantities and the block NLL
  *   dbl_expand_branches / dbl_prior_head  the head's inputs: branch states and category logits
+ *   dbl_target_logprobs / dbl_early_determinism  the target side: the sampling transform that
+ *                       defines p, and the target-block early-determinism estimate
  *
  * and the same three steps for the greedy-branch proposal that the paper's reported
  * experiments use (appendix "Greedy-Branch Proposal"): dbl_sample_greedy, dbl_verify_greedy,
@@ -317,6 +319,37 @@ dbl_status dbl_expand_branches(dbl_shape shape, const void* h, const void* W, co
  */
 dbl_status dbl_prior_head(dbl_shape shape, const void* h_anchor, const void* U, const void* e,
                           float* prior_logits, void* stream);
+
+/*
+ * dbl_target_logprobs - the target's sampling distribution as log-probabilities, the p of every
+ * verification and objective call (Sec. "Acceptance-Oriented Training": the same temperature,
+ * top-k and top-p transform generates the trajectories and enters the acceptance probabilities).
+ * Per row: s = fl32(logit / T); top-k (k > 0) keeps every id whose s is at least the k-th largest
+ * value (ties at the cut are kept); top-p (p < 1) then keeps, visiting the kept ids by decreasing
+ * s and increasing id, each id while the integer mass sum floor(detexp32(fl32(s - max)) 2^40) of
+ * the ids before it is below ceil(p * total) (binary64 product); log p = s - max - log(sum over
+ * kept of exp(s - max)) in binary64, -inf outside the kept set. T = 0 keeps only the lowest-index
+ * maximum (log p = 0 there). The kept set is exact and independent of evaluation order.
+ *   N, V         rows and vocabulary size (1 <= V < 2^24)
+ *   logits       [N, V] fp32 target logits;  logp  out [N, V] fp32 (may alias logits)
+ *   temperature  finite, >= 0;  top_k  >= 0 (0: off);  top_p  in (0, 1] (1: off)
+ * No workspace. Errors: DBL_EINVAL for null pointers or parameters out of range; DBL_ESHAPE.
+ */
+dbl_status dbl_target_logprobs(int64_t N, int64_t V, const float* logits, float temperature,
+                               int64_t top_k, float top_p, float* logp, void* stream);
+
+/*
+ * dbl_early_determinism - target-block early determinism (appendix "Target-Block Early
+ * Determinism"): from M blocks x[m] of length b sampled from the target, with p_i the target
+ * distribution at position i of block m (row (m*b + i) of logp),
+ *     terms[m] = (1/b) sum_{j<=b} prod_{i<=j} p_i(x[m, i]),   mean = (1/M) sum_m terms[m],
+ * the estimate of D_b = (1/b) sum_j sum_{u in V^j} p(u)^2. Binary64 accumulation.
+ *   x     [M, b] int32 (ids outside [0, V) have probability 0);  logp [M, b, V] fp32
+ *   terms out [M] fp32;  mean out scalar fp32 (device) or NULL
+ * No workspace. Errors: DBL_EINVAL for null pointers; DBL_ESHAPE.
+ */
+dbl_status dbl_early_determinism(int64_t M, int64_t b, int64_t V, const int32_t* x,
+                                 const float* logp, float* terms, float* mean, void* stream);
 
 #ifdef __cplusplus
 }

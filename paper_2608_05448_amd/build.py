@@ -27,6 +27,7 @@ SOURCES = {
     "verify.hip": ["-ffp-contract=off"],
     "greedy.hip": ["-ffp-contract=off"],
     "objective.hip": [],
+    "target.hip": ["-ffp-contract=off"],
 }
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -424,4 +424,45 @@ dbl_status dbl_prior_head(dbl_shape s, const void* h_anchor, const void* U, cons
                     "prior head launch");
 }
 
+dbl_status dbl_target_logprobs(int64_t N, int64_t V, const float* logits, float temperature,
+                               int64_t top_k, float top_p, float* logp, void* stream) {
+  if (N < 0 || V < 1 || V >= (int64_t(1) << 24)) return fail(DBL_ESHAPE, "need N >= 0, 1 <= V < 2^24");
+  if (static_cast<double>(N) * static_cast<double>(V) >= 4.0e18)
+    return fail(DBL_ESHAPE, "N*V too large");
+  if (!logits || !logp) return fail(DBL_EINVAL, "NULL pointer");
+  if (!(temperature >= 0.0f) || isinf(temperature))
+    return fail(DBL_EINVAL, "temperature must be finite and >= 0");
+  if (top_k < 0) return fail(DBL_EINVAL, "top_k must be >= 0");
+  if (!(top_p > 0.0f && top_p <= 1.0f)) return fail(DBL_EINVAL, "top_p must be in (0, 1]");
+  if (N == 0) return ok();
+  dbl::FilterArgs a;
+  a.N = N;
+  a.V = V;
+  a.logits = logits;
+  a.temperature = temperature;
+  a.top_k = top_k;
+  a.top_p = top_p;
+  a.logp = logp;
+  return hip_status(dbl::launch_filter(a, static_cast<hipStream_t>(stream)), "filter launch");
+}
+
+dbl_status dbl_early_determinism(int64_t M, int64_t b, int64_t V, const int32_t* x,
+                                 const float* logp, float* terms, float* mean, void* stream) {
+  if (M < 0 || b < 1 || V < 1 || V >= (int64_t(1) << 24))
+    return fail(DBL_ESHAPE, "need M >= 0, b >= 1, 1 <= V < 2^24");
+  if (static_cast<double>(M) * b * V >= 4.0e18) return fail(DBL_ESHAPE, "M*b*V too large");
+  if (!x || !logp || !terms) return fail(DBL_EINVAL, "NULL pointer");
+  if (M == 0) return ok();
+  dbl::DeterminismArgs a;
+  a.M = M;
+  a.b = b;
+  a.V = V;
+  a.x = x;
+  a.logp = logp;
+  a.terms = terms;
+  a.mean = mean;
+  return hip_status(dbl::launch_determinism(a, static_cast<hipStream_t>(stream)),
+                    "early determinism launch");
+}
+
 }  // extern "C"

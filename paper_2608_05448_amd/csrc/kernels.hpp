@@ -114,6 +114,25 @@ struct PriorHeadArgs {
   float* ell;            // [B, R]
 };
 
+// Target sampling transform: rows of logits -> filtered log-probabilities.
+struct FilterArgs {
+  int64_t N, V;
+  const float* logits;  // [N, V]
+  float temperature;
+  int64_t top_k;        // 0: off
+  float top_p;          // 1: off
+  float* logp;          // [N, V]
+};
+
+// Early-determinism estimate from sampled target blocks.
+struct DeterminismArgs {
+  int64_t M, b, V;
+  const int32_t* x;     // [M, b]
+  const float* logp;    // [M, b, V]
+  float* terms;         // [M]
+  float* mean;          // scalar or null
+};
+
 inline int n_chunks(int nT) { return (nT + kTilesPerChunk - 1) / kTilesPerChunk; }
 
 hipError_t launch_head(const HeadArgs& a, hipStream_t stream);
@@ -124,5 +143,7 @@ hipError_t launch_verify_greedy(const GreedyArgs& a, hipStream_t stream);
 hipError_t launch_objective(const ObjectiveArgs& a, hipStream_t stream);
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
 hipError_t launch_prior_head(const PriorHeadArgs& a, hipStream_t stream);
+hipError_t launch_filter(const FilterArgs& a, hipStream_t stream);
+hipError_t launch_determinism(const DeterminismArgs& a, hipStream_t stream);
 
 }  // namespace dbl

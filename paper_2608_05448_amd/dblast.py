@@ -61,6 +61,8 @@ _SIGS = {
                                                 _P, _P, _P, _P]),
     "dbl_expand_branches": (ctypes.c_int, [Shape, _P, _P, _P, _P, _P]),
     "dbl_prior_head": (ctypes.c_int, [Shape, _P, _P, _P, _P, _P]),
+    "dbl_target_logprobs": (ctypes.c_int, [_I64, _I64, _P, _F, _I64, _F, _P, _P]),
+    "dbl_early_determinism": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -370,3 +372,29 @@ def dbl_prior_head(h_anchor, U, e, out=None):
     _check(load().dbl_prior_head(Shape(B, 1, R, d, 1), _ptr(h_anchor), _ptr(U), _ptr(e),
                                  _ptr(out), _stream(dev)))
     return out
+
+
+def dbl_target_logprobs(logits, temperature=1.0, top_k=0, top_p=1.0, out=None):
+    """Target sampling log-probabilities for logits [..., V] fp32 (temperature, top-k, top-p)."""
+    _need(logits, "logits", torch.float32)
+    V = logits.shape[-1]
+    N = logits.numel() // V
+    out = torch.empty_like(logits) if out is None else out
+    _need(out, "out", torch.float32, tuple(logits.shape))
+    _check(load().dbl_target_logprobs(N, V, _ptr(logits), float(temperature), int(top_k),
+                                      float(top_p), _ptr(out), _stream(logits.device)))
+    return out
+
+
+def dbl_early_determinism(x, logp):
+    """Early-determinism estimate from sampled target blocks x [M, b] and their target
+    log-probs logp [M, b, V]: returns (terms [M], mean [] ) fp32 tensors."""
+    M, b = x.shape
+    _need(x, "x", torch.int32)
+    _need(logp, "logp", torch.float32, (M, b, logp.shape[-1]))
+    dev = x.device
+    terms = torch.empty(M, dtype=torch.float32, device=dev)
+    mean = torch.empty((), dtype=torch.float32, device=dev)
+    _check(load().dbl_early_determinism(M, b, logp.shape[-1], _ptr(x), _ptr(logp), _ptr(terms),
+                                        _ptr(mean), _stream(dev)))
+    return terms, mean

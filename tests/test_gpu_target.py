@@ -1,0 +1,94 @@
+"""GPU parity of dbl_target_logprobs and dbl_early_determinism against the oracle.
+
+The kept set of every row (which ids are finite) must be identical: both cuts are integer
+decisions on binary32 values computed the same way on both sides. Log-probabilities of kept ids
+agree within 2e-6 (binary64 normaliser summed in a different order, stored as binary32).
+"""
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import target as TG
+
+pytestmark = pytest.mark.gpu
+
+
+def _logits(N, V, seed, ties=False):
+    g = synth.make_uniform_logits((N, V), seed, scale=3.0).numpy()
+    perm = np.random.default_rng(seed).permutation(V)
+    g = g - 1.1 * np.log1p(perm)[None, :]
+    if ties:   # coarse values: many equal logits at both cuts
+        g = np.round(g * 2.0) / 2.0
+    return g.astype(np.float32)
+
+
+CASES = [
+    # name, N, V, T, top_k, top_p, ties
+    ("paper-t07-k20-p08", 6, 151936, 0.7, 20, 0.8, False),
+    ("paper-t10-k20-p095", 6, 151936, 1.0, 20, 0.95, False),
+    ("paper-t15-k20-p095", 6, 151936, 1.5, 20, 0.95, False),
+    ("greedy", 5, 151936, 0.0, 20, 0.95, False),
+    ("nucleus-only", 4, 151936, 1.0, 0, 0.9, False),
+    ("top-k-only", 4, 50000, 1.0, 50, 1.0, False),
+    ("no-filter", 3, 3001, 1.3, 0, 1.0, False),
+    ("ties-at-both-cuts", 16, 2000, 1.0, 30, 0.7, True),
+    ("ties-nucleus-only", 16, 2000, 1.0, 0, 0.5, True),
+    ("tiny-vocab", 8, 7, 1.0, 3, 0.6, True),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_target_filter_parity(case):
+    from paper_2608_05448_amd import dblast as D
+    name, N, V, T, k, p, ties = case
+    print(f"[target] {name} N={N} V={V} T={T} k={k} p={p}", flush=True)
+    lg = _logits(N, V, 7 + len(name), ties)
+    got = D.dbl_target_logprobs(torch.from_numpy(lg).cuda(), T, k, p)
+    torch.cuda.synchronize()
+    got = got.cpu().numpy()
+    want = TG.filter_logprobs(lg, T, k, p)
+    assert np.array_equal(np.isfinite(got), np.isfinite(want))
+    fin = np.isfinite(want)
+    assert np.max(np.abs(got[fin] - want[fin])) < 2e-6
+    print(f"[target] {name}: kept per row {np.isfinite(want).sum(1).tolist()}", flush=True)
+
+
+def test_target_filter_benchmark_rows():
+    """The Qwen3-8B verification rows (16 blocks x 17 positions) with the paper's filters."""
+    from paper_2608_05448_amd import dblast as D
+    N, V = 272, 151936
+    lg = torch.from_numpy(_logits(N, V, 99)).cuda()
+    out = torch.empty_like(lg)
+    for T, k, p in ((0.7, 20, 0.8), (1.0, 20, 0.95), (1.0, 0, 0.95)):
+        D.dbl_target_logprobs(lg, T, k, p, out=out)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(5):
+            D.dbl_target_logprobs(lg, T, k, p, out=out)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) / 5 * 1e3
+        print(f"[target] rows {N} x {V}, T={T} k={k} p={p}: {ms:.3f} ms "
+              f"({N * V * 8 / ms / 1e6:.0f} GB/s of logits in + logp out)", flush=True)
+    rows = [0, 135, 271]
+    want = TG.filter_logprobs(lg[rows].cpu().numpy(), 1.0, 0, 0.95)
+    got = out[rows].cpu().numpy()
+    assert np.array_equal(np.isfinite(got), np.isfinite(want))
+
+
+def test_early_determinism_parity():
+    from paper_2608_05448_amd import dblast as D
+    M, b, V = 300, 8, 500
+    lp = TG.filter_logprobs(_logits(M * b, V, 5), 1.0, 20, 0.9).reshape(M, b, V)
+    rng = np.random.default_rng(6)
+    p = np.exp(lp.astype(np.float64))
+    cum = np.cumsum(p / p.sum(-1, keepdims=True), -1)
+    x = np.minimum((cum < rng.random((M, b, 1))).sum(-1), V - 1).astype(np.int32)
+    terms, mean = D.dbl_early_determinism(torch.from_numpy(x).cuda(), torch.from_numpy(lp).cuda())
+    torch.cuda.synchronize()
+    lpx = lp[np.arange(M)[:, None], np.arange(b)[None, :], x]
+    want_terms = np.exp(np.cumsum(lpx.astype(np.float64), axis=1)).mean(1)
+    np.testing.assert_allclose(terms.cpu().numpy(), want_terms, rtol=1e-6, atol=1e-9)
+    assert abs(mean.item() - TG.early_determinism(lpx)) < 1e-6
