@@ -100,16 +100,24 @@ __device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], f
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int o = rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          if (o < vlim && acc[rb][cb][r] > mx) {
-            mx = acc[rb][cb][r];
-            vi = o;
+          if constexpr (ARG) {
+            if (o < vlim && acc[rb][cb][r] > mx) {
+              mx = acc[rb][cb][r];
+              vi = o;
+            }
+          } else {
+            if (o < vlim) mx = fmaxf(mx, acc[rb][cb][r]);
           }
         }
-      const float omx = __shfl_xor(mx, 32);
-      const int ovi = __shfl_xor(vi, 32);
-      if (omx > mx || (omx == mx && ovi < vi)) {
-        mx = omx;
-        vi = ovi;
+      if constexpr (ARG) {
+        const float omx = __shfl_xor(mx, 32);
+        const int ovi = __shfl_xor(vi, 32);
+        if (omx > mx || (omx == mx && ovi < vi)) {
+          mx = omx;
+          vi = ovi;
+        }
+      } else {
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
       }
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb)
