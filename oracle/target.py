@@ -18,7 +18,7 @@ here (and by the GPU library) is:
   all kept);
 * top-p (p < 1) on the kept set: with m the maximum and the integer masses
   P(v) = floor(detexp32(fl32(s(v) - m)) * 2^40) of the determinism contract, Z their sum over the
-  kept set and T_p = ceil(p * Z) (binary64 product), the kept tokens are visited by decreasing s
+  kept set and T_p = ceil(p * Z) (binary64 product of the binary32 p), the kept tokens are visited by decreasing s
   and, among equal s, increasing id; a token is kept while the mass of the tokens before it is
   below T_p (the first token is always kept);
 * log p(v) = s(v) - m - log(sum over kept u of exp(s(u) - m)) in binary64, stored as binary32.
@@ -56,7 +56,7 @@ def filter_logprobs(logits, temperature: float, top_k: int = 0, top_p: float = 1
             order = idx[np.lexsort((idx, -row[idx].astype(np.float64)))]
             P = quant40(detexp32((row[order] - m).astype(np.float32))).astype(object)
             Z = int(sum(P))
-            Tp = int(np.ceil(np.float64(top_p) * np.float64(Z)))
+            Tp = max(1, int(np.ceil(np.float64(np.float32(top_p)) * np.float64(Z))))
             before = 0
             kept = []
             for v, pv in zip(order, P):
