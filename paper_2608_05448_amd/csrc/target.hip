@@ -88,8 +88,245 @@ __device__ __forceinline__ void pick_digit(const uint64_t* hist, uint64_t need, 
   __syncthreads();
 }
 
+// Calls fn(v, logit(v)) for every id of the row. When the row is 16-byte aligned and V is a
+// multiple of 4 the loads are float4, issued kB at a time per thread so that one workgroup keeps
+// enough bytes in flight to stream its row.
+constexpr int kBatch = 8;
+
+template <int kB = kBatch, class F>
+__device__ __forceinline__ void row_scan_raw(const float* in, int64_t V, bool vec, F fn) {
+  if (vec) {
+    const float4* in4 = reinterpret_cast<const float4*>(in);
+    const int64_t n4 = V >> 2;
+    auto one = [&](int64_t j, const float4& x) {
+      fn(4 * j, x.x);
+      fn(4 * j + 1, x.y);
+      fn(4 * j + 2, x.z);
+      fn(4 * j + 3, x.w);
+    };
+    int64_t j = threadIdx.x;
+    for (; j + (kB - 1) * kFT < n4; j += kB * kFT) {
+      float4 x[kB];
+#pragma unroll
+      for (int u = 0; u < kB; ++u) x[u] = in4[j + u * kFT];
+#pragma unroll
+      for (int u = 0; u < kB; ++u) one(j + u * kFT, x[u]);
+    }
+    for (; j < n4; j += kFT) one(j, in4[j]);
+  } else {
+    for (int64_t v = threadIdx.x; v < V; v += kFT) fn(v, in[v]);
+  }
+}
+
+// As row_scan_raw, with fn(v, s(v)), s(v) = fl32(logit(v) / T).
+template <int kB = kBatch, class F>
+__device__ __forceinline__ void row_scan(const float* in, int64_t V, float T, bool vec, F fn) {
+  row_scan_raw<kB>(in, V, vec, [&](int64_t v, float x) { fn(v, __fdiv_rn(x, T)); });
+}
+
+__device__ __forceinline__ float key_value(uint32_t x) {
+  return __uint_as_float((x & 0x80000000u) ? (x & 0x7FFFFFFFu) : ~x);
+}
+
+constexpr uint32_t kKeyNegInf = 0x007FFFFFu;  // order_key(-inf)
+constexpr uint32_t kKeyPosInf = 0xFF800000u;  // order_key(+inf)
+
+// Rounded division by T > 0 is monotone (non-decreasing) in the dividend, so the logits x with
+// fl32(x / T) >= s form an upper set in key order. Returns its least key: a bisection over the
+// keys of the non-NaN floats, every thread computing the same value.
+__device__ __forceinline__ uint32_t least_logit_key(uint32_t s_key, float T) {
+  auto ok = [&](uint32_t k) { return order_key(__fdiv_rn(key_value(k), T)) >= s_key; };
+  if (ok(kKeyNegInf)) return kKeyNegInf;
+  uint32_t lo = kKeyNegInf, hi = kKeyPosInf;  // ok(lo) false, ok(hi) true
+  while (hi - lo > 1) {
+    const uint32_t mid = lo + (hi - lo) / 2;
+    if (ok(mid)) hi = mid; else lo = mid;
+  }
+  return hi;
+}
+
+// Sort key of a token: key(s) in the high word, ~id in the low word, so that a descending order
+// visits tokens by decreasing s and, among equal s, increasing id.
+__device__ __forceinline__ uint64_t visit_key(uint32_t key, int64_t v) {
+  return (static_cast<uint64_t>(key) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(v));
+}
+
+// Fast path for top-k (0 < k <= kFastK < V): three streaming passes over the row instead of up
+// to ten, none of which divides more than a few candidates (fl32(x / T) is monotone in x, so
+// selections on s can be made on the logits' keys):
+//   1. every thread keeps the four largest logit keys it sees; the k-th largest t of these 4096
+//      keys (found by bisection) is at most the row's k-th largest, the union being part of
+//      the row, so s_t = fl32(t / T) is at most the k-th largest s;
+//   2. every token with s >= s_t (logit key at least least_logit_key(s_t)) is appended to an
+//      LDS list with its s;
+//   3. the list is sorted in visiting order; both cuts and the normaliser follow from it, and a
+//      token is kept iff its visiting key is at least that of the last kept token;
+//   4. the output row is written; only logits at or above the cut's least key are divided.
+// Returns false (the caller then runs the radix path) if the list would overflow LDS.
+constexpr int kFastK = 1024;
+constexpr int kCandCap = 4096;
+
+__device__ bool filter_fast(const FilterArgs& a, const float* in, float* out, bool vec,
+                            uint64_t* cand, uint64_t* red, double* redd, int* sh_n) {
+  const int tid = threadIdx.x;
+  const int64_t V = a.V;
+  const float T = a.temperature;
+  const int k = static_cast<int>(a.top_k);
+  // 1. per-thread top-4 logit keys
+  uint32_t t0 = 0, t1 = 0, t2 = 0, t3 = 0;
+  row_scan_raw(in, V, vec, [&](int64_t, float lv) {
+    uint32_t x = order_key(lv);  // insertion into t0 >= t1 >= t2 >= t3, branch-free
+    uint32_t y = max(t0, x);
+    x = min(t0, x);
+    t0 = y;
+    y = max(t1, x);
+    x = min(t1, x);
+    t1 = y;
+    y = max(t2, x);
+    x = min(t2, x);
+    t2 = y;
+    t3 = max(t3, x);
+  });
+  // k-th largest of the union: largest t with at least k union entries >= t (t = 0 always has
+  // all 4096, and 4096 >= k).
+  uint64_t lo = 0, hi = block_max_u64(t0, red);
+  while (lo < hi) {
+    const uint64_t mid = lo + (hi - lo + 1) / 2;
+    const uint32_t m32 = static_cast<uint32_t>(mid);
+    const uint32_t c = __popcll(__ballot(t0 >= m32)) + __popcll(__ballot(t1 >= m32)) +
+                       __popcll(__ballot(t2 >= m32)) + __popcll(__ballot(t3 >= m32));
+    if (lane_id() == 0) red[tid >> 6] = c;
+    __syncthreads();
+    uint64_t tot = 0;
+#pragma unroll
+    for (int w = 0; w < kFW; ++w) tot += red[w];
+    __syncthreads();
+    if (tot >= static_cast<uint64_t>(k)) lo = mid; else hi = mid - 1;
+  }
+  const uint32_t s_low = order_key(__fdiv_rn(key_value(static_cast<uint32_t>(lo)), T));
+  const uint32_t x_low = least_logit_key(s_low, T);
+  // 2. append every token with s >= s_t
+  if (tid == 0) *sh_n = 0;
+  __syncthreads();
+  row_scan_raw(in, V, vec, [&](int64_t v, float lv) {
+    if (order_key(lv) >= x_low) {
+      const int slot = atomicAdd(sh_n, 1);
+      if (slot < kCandCap) cand[slot] = visit_key(order_key(__fdiv_rn(lv, T)), v);
+    }
+  });
+  __syncthreads();
+  const int n = *sh_n;
+  __syncthreads();
+  if (n > kCandCap) return false;
+  // 3. bitonic sort, descending, of the list padded with zeros to a power of two (every real
+  //    entry has a nonzero low word, ids being below 2^32 - 1)
+  int np = 64;
+  while (np < n) np <<= 1;
+  for (int i = n + tid; i < np; i += kFT) cand[i] = 0;
+  __syncthreads();
+  for (int size = 2; size <= np; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < (np >> 1); i += kFT) {
+        const int i0 = 2 * i - (i & (stride - 1));  // the pair (i0, i0 + stride)
+        const int i1 = i0 + stride;
+        const bool desc = (i0 & size) == 0;
+        const uint64_t x = cand[i0], y = cand[i1];
+        if ((x < y) == desc) {
+          cand[i0] = y;
+          cand[i1] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  auto key_at = [&](int i) { return static_cast<uint32_t>(cand[i] >> 32); };
+  const float m = key_value(key_at(0));
+  // top-k: the first k entries and every later one tied with the k-th (n >= k: the list holds
+  // every token at or above the row's k-th largest key)
+  const uint32_t tk = key_at(k - 1);
+  int nk = k;
+  while (nk < n && key_at(nk) >= tk) ++nk;
+  int nkeep = nk;
+  if (a.top_p < 1.0f) {
+    // integer masses of the first nk entries, four per thread in list order; a token is kept
+    // while the mass before it is below T_p = ceil(p Z)
+    uint64_t P[4], loc = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = 4 * tid + j;
+      P[j] = i < nk ? quant40(detexp32(__fsub_rn(key_value(key_at(i)), m))) : 0;
+      loc += P[j];
+    }
+    const uint64_t incl = wave_incl_scan_u64(loc);
+    if (lane_id() == 63) red[tid >> 6] = incl;
+    __syncthreads();
+    uint64_t base = 0, z = 0;
+#pragma unroll
+    for (int w = 0; w < kFW; ++w) {
+      const uint64_t r = red[w];
+      base += w < (tid >> 6) ? r : 0;
+      z += r;
+    }
+    __syncthreads();
+    uint64_t tp = static_cast<uint64_t>(ceil(__dmul_rn(static_cast<double>(a.top_p),
+                                                       static_cast<double>(z))));
+    if (tp == 0) tp = 1;
+    uint64_t before = base + incl - loc;
+    uint64_t c = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (4 * tid + j < nk) {
+        c += before < tp ? 1 : 0;
+        before += P[j];
+      }
+    }
+    nkeep = static_cast<int>(block_sum_u64(c, red));
+  }
+  const uint64_t cut = cand[nkeep - 1];
+  double se = 0.0;
+  for (int i = tid; i < nkeep; i += kFT)
+    se += exp(static_cast<double>(key_value(key_at(i))) - static_cast<double>(m));
+  const double lse = log(block_sum_f64(se, redd));
+  // 4. output row
+  const uint32_t x_cut = least_logit_key(static_cast<uint32_t>(cut >> 32), T);
+  auto val = [&](int64_t v, float lv) {
+    if (order_key(lv) < x_cut) return -INFINITY;
+    const float sv = __fdiv_rn(lv, T);
+    return visit_key(order_key(sv), v) >= cut
+               ? static_cast<float>(static_cast<double>(sv) - static_cast<double>(m) - lse)
+               : -INFINITY;
+  };
+  if (vec) {
+    const float4* in4 = reinterpret_cast<const float4*>(in);
+    float4* out4 = reinterpret_cast<float4*>(out);
+    const int64_t n4 = V >> 2;
+    auto one = [&](int64_t j, const float4& x) {
+      float4 y;
+      y.x = val(4 * j, x.x);
+      y.y = val(4 * j + 1, x.y);
+      y.z = val(4 * j + 2, x.z);
+      y.w = val(4 * j + 3, x.w);
+      out4[j] = y;
+    };
+    int64_t j = tid;
+    for (; j + (kBatch - 1) * kFT < n4; j += kBatch * kFT) {
+      float4 x[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) x[u] = in4[j + u * kFT];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) one(j + u * kFT, x[u]);
+    }
+    for (; j < n4; j += kFT) one(j, in4[j]);
+  } else {
+    for (int64_t v = tid; v < V; v += kFT) out[v] = val(v, in[v]);
+  }
+  return true;
+}
+
 __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
   __shared__ uint64_t hist[256];
+  __shared__ uint64_t cand[kCandCap];
+  __shared__ int sh_n;
   __shared__ uint64_t red[kFW];
   __shared__ double redd[kFW];
   __shared__ uint32_t sh_digit;
@@ -114,13 +351,18 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
   }
   const float T = a.temperature;
   auto s_of = [&](int64_t v) { return __fdiv_rn(in[v], T); };
+  const bool vec = (V & 3) == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  if (a.top_k > 0 && a.top_k <= kFastK && a.top_k < V &&
+      filter_fast(a, in, out, vec, cand, red, redd, &sh_n))
+    return;
 
   // Row maximum (key of the largest s).
-  uint64_t mk = 0;
-  for (int64_t v = tid; v < V; v += kFT) {
-    const uint64_t k = order_key(s_of(v));
+  uint32_t mk = 0;
+  row_scan<4>(in, V, T, vec, [&](int64_t, float sv) {
+    const uint32_t k = order_key(sv);
     mk = k > mk ? k : mk;
-  }
+  });
   const uint32_t max_key = static_cast<uint32_t>(block_max_u64(mk, red));
   const float m = __uint_as_float((max_key & 0x80000000u) ? (max_key & 0x7FFFFFFFu) : ~max_key);
 
@@ -132,10 +374,11 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
     for (int shift = 24; shift >= 0; shift -= 8) {
       for (int i = tid; i < 256; i += kFT) hist[i] = 0;
       __syncthreads();
-      for (int64_t v = tid; v < V; v += kFT) {
-        const uint32_t k = order_key(s_of(v));
-        if ((k & pmask) == prefix) atomicAdd(reinterpret_cast<unsigned long long*>(&hist[(k >> shift) & 255]), 1ull);
-      }
+      row_scan<4>(in, V, T, vec, [&](int64_t, float sv) {
+        const uint32_t k = order_key(sv);
+        if ((k & pmask) == prefix)
+          atomicAdd(reinterpret_cast<unsigned long long*>(&hist[(k >> shift) & 255]), 1ull);
+      });
       __syncthreads();
       uint32_t d;
       uint64_t above;
@@ -151,22 +394,22 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
   uint32_t tp = 0;          // keep keys > tp, and the first n_tie tokens with key == tp
   uint64_t n_tie = ~0ull;
   if (a.top_p < 1.0f) {
-    auto mass = [&](int64_t v, uint32_t k) -> uint64_t {
-      return k >= tk ? quant40(detexp32(__fsub_rn(s_of(v), m))) : 0;
+    auto mass = [&](float sv, uint32_t k) -> uint64_t {
+      return k >= tk ? quant40(detexp32(__fsub_rn(sv, m))) : 0;
     };
     uint32_t prefix = 0, pmask = 0;
     uint64_t need = 0, tie_mass = 0;
     for (int shift = 24; shift >= 0; shift -= 8) {
       for (int i = tid; i < 256; i += kFT) hist[i] = 0;
       __syncthreads();
-      for (int64_t v = tid; v < V; v += kFT) {
-        const uint32_t k = order_key(s_of(v));
+      row_scan<4>(in, V, T, vec, [&](int64_t, float sv) {
+        const uint32_t k = order_key(sv);
         if ((k & pmask) == prefix) {
-          const uint64_t P = mass(v, k);
+          const uint64_t P = mass(sv, k);
           if (P) atomicAdd(reinterpret_cast<unsigned long long*>(&hist[(k >> shift) & 255]),
                            static_cast<unsigned long long>(P));
         }
-      }
+      });
       __syncthreads();
       if (shift == 24) {  // total mass of the kept set: T_p = ceil(p Z)
         uint64_t z = 0;
@@ -186,7 +429,7 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
     tp = prefix;
     // Every token at key tp has the same mass; count how many of them there are.
     uint64_t cnt = 0;
-    for (int64_t v = tid; v < V; v += kFT) cnt += order_key(s_of(v)) == tp ? 1 : 0;
+    row_scan<4>(in, V, T, vec, [&](int64_t, float sv) { cnt += order_key(sv) == tp ? 1 : 0; });
     cnt = block_sum_u64(cnt, red);
     const uint64_t each = tie_mass / cnt;
     n_tie = (need + each - 1) / each;  // tokens at tp needed to reach T_p
@@ -223,23 +466,22 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
   // some of the tokens at the top-p cut are kept, which needs the id-ordered runs.
   auto pass = [&](auto fn) {
     if (n_tie == ~0ull) {
-      for (int64_t v = tid; v < V; v += kFT) fn(v, 0ull);
+      row_scan<4>(in, V, T, vec, [&](int64_t v, float sv) { fn(v, sv, 0ull); });
     } else {
       uint64_t rank = tie_before;
       for (int64_t v = r0; v < r1; ++v) {
-        fn(v, rank);
-        if (order_key(s_of(v)) == tp) ++rank;
+        const float sv = s_of(v);
+        fn(v, sv, rank);
+        if (order_key(sv) == tp) ++rank;
       }
     }
   };
   double se = 0.0;
-  pass([&](int64_t v, uint64_t rank) {
-    const float s = s_of(v);
+  pass([&](int64_t v, float s, uint64_t rank) {
     if (kept(v, order_key(s), rank)) se += exp(static_cast<double>(s) - static_cast<double>(m));
   });
   const double lse = log(block_sum_f64(se, redd));
-  pass([&](int64_t v, uint64_t rank) {
-    const float s = s_of(v);
+  pass([&](int64_t v, float s, uint64_t rank) {
     out[v] = kept(v, order_key(s), rank)
                  ? static_cast<float>(static_cast<double>(s) - static_cast<double>(m) - lse)
                  : -INFINITY;

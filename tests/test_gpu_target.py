@@ -17,10 +17,17 @@ pytestmark = pytest.mark.gpu
 
 
 def _logits(N, V, seed, ties=False):
+    if ties == "flat":   # every logit equal: top-k keeps the whole row
+        return np.zeros((N, V), np.float32)
     g = synth.make_uniform_logits((N, V), seed, scale=3.0).numpy()
     perm = np.random.default_rng(seed).permutation(V)
     g = g - 1.1 * np.log1p(perm)[None, :]
-    if ties:   # coarse values: many equal logits at both cuts
+    if ties == "ulp":   # the 40 largest logits one ulp apart: fl32(x / T) merges neighbours
+        g = g.astype(np.float32)
+        for r in range(N):
+            top = np.argsort(-g[r])[:40]
+            g[r, top] = np.float32(7.0) + np.arange(40, dtype=np.float32) * np.spacing(np.float32(7.0))
+    elif ties:   # coarse values: many equal logits at both cuts
         g = np.round(g * 2.0) / 2.0
     return g.astype(np.float32)
 
@@ -37,6 +44,15 @@ CASES = [
     ("ties-at-both-cuts", 16, 2000, 1.0, 30, 0.7, True),
     ("ties-nucleus-only", 16, 2000, 1.0, 0, 0.5, True),
     ("tiny-vocab", 8, 7, 1.0, 3, 0.6, True),
+    ("top-k-ragged-row", 4, 50001, 1.0, 50, 0.9, False),
+    ("top-k-1000-ties", 4, 151936, 1.0, 1000, 0.9, True),
+    ("top-k-1024", 3, 151936, 1.2, 1024, 0.95, False),
+    ("top-k-1025", 3, 151936, 1.2, 1025, 0.95, False),
+    ("flat-row-top-k", 2, 151936, 1.0, 20, 0.95, "flat"),
+    ("one-ulp-neighbours-t15", 4, 30000, 1.5, 20, 0.95, "ulp"),
+    ("one-ulp-neighbours-t07", 4, 30000, 0.7, 20, 0.95, "ulp"),
+    ("temperature-3e4-merges-values", 4, 30000, 3e4, 20, 0.95, False),
+    ("temperature-1e-3", 4, 30000, 1e-3, 20, 0.9, False),
 ]
 
 
@@ -62,7 +78,7 @@ def test_target_filter_benchmark_rows():
     N, V = 272, 151936
     lg = torch.from_numpy(_logits(N, V, 99)).cuda()
     out = torch.empty_like(lg)
-    for T, k, p in ((0.7, 20, 0.8), (1.0, 20, 0.95), (1.0, 0, 0.95)):
+    for T, k, p in ((0.7, 20, 0.8), (1.0, 20, 0.95), (1.5, 20, 1.0), (1.0, 0, 0.95)):
         D.dbl_target_logprobs(lg, T, k, p, out=out)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
