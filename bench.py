@@ -1,7 +1,7 @@
 """Throughput of the DBLast head + block draw + verification on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen3_8b]
-                    [--temperature T] [--mode soft|greedy] [--no-cpu-baseline]
+                    [--temperature T] [--mode soft|greedy|rows] [--no-cpu-baseline]
                     [--copy-calibration BYTES]
 
 One step is one pass of the whole hot path over one batch of synthetic inputs already resident
@@ -10,6 +10,9 @@ and token draw) and dbl_verify_block (posterior, accept test, residual/bonus dra
 masses, AL_b and E). The Philox step counter advances every step. Prints one JSON line.
 With --mode greedy the step is the greedy-branch variant: the head also returns each row's
 argmax, then dbl_sample_greedy and dbl_verify_greedy.
+With --mode rows the line instead times the other entry points at the workload's shape (branch
+expander, prior head, objective forward, target transform, early-determinism estimate), each
+against its own bound; it is a measurement aid, not the step metric.
 
 The metric is verified block positions per second, B*K / step time. The roofline entry is for
 the dominant kernel, the head GEMM: 2*M*d*V flops per launch over its average launch time,
@@ -148,6 +151,81 @@ def _copy_calibration(nbytes: int):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
 
 
+def _rows(wl, dev, steps: int, warmup: int):
+    """Average time per call (HIP events on the library's stream) of the entry points outside
+    the step, at the workload's shape, each with its algorithmic bytes or flops and bound."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_05448_amd import dblast as D
+
+    B, K, R, d, V = wl.B, wl.K, wl.R, wl.d, wl.V
+    stream = torch.cuda.current_stream(dev)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize(dev)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        return e0.elapsed_time(e1) / steps
+
+    def hbm(ms, nbytes):
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        return {"ms": ms, "bound": "hbm", "bytes": nbytes, "achieved": gbs,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS}
+
+    rows = {}
+    # Branch expander: [B*K, d] x [R*d, d]^T plus bias and residual, bf16 out.
+    ht = synth.make_uniform_logits((B, K, d), 11, device=dev).to(torch.bfloat16)
+    We = (synth.make_uniform_logits((R * d, d), 12, device=dev) * (0.5 / d ** 0.5)).to(torch.bfloat16)
+    ce = (synth.make_uniform_logits((R * d,), 13, device=dev) * 0.1).to(torch.bfloat16)
+    hb = torch.empty((B, K, R, d), dtype=torch.bfloat16, device=dev)
+    ms = timed(lambda: D.dbl_expand_branches(ht, We, ce, R, out=hb))
+    r = hbm(ms, 2.0 * (R * d * d + B * K * d + R * d + B * K * R * d))
+    r["tflops"] = 2.0 * B * K * R * d * d / (ms * 1e-3) / 1e12
+    rows["expand_branches"] = r
+    # Prior head: category logits from the anchor states.
+    U = (synth.make_uniform_logits((R, d), 14, device=dev) * (1.0 / d ** 0.5)).to(torch.bfloat16)
+    e = (synth.make_uniform_logits((R,), 15, device=dev) * 0.1).to(torch.bfloat16)
+    pl = torch.empty((B, R), dtype=torch.float32, device=dev)
+    ha = ht[:, 0].contiguous()
+    ms = timed(lambda: D.dbl_prior_head(ha, U, e, out=pl))
+    rows["prior_head"] = {"ms": ms, "bound": "latency"}
+    # Objective forward along target trajectories (head outputs of the step's inputs).
+    h = synth.make_h(wl, dev)
+    w = synth.make_w(wl, dev)
+    tls, lmass, lse = D.dbl_head_logprobs(h, w)
+    del w
+    ell = synth.make_ell(wl, dev)
+    logp = synth.make_logp(wl, rows=K, device=dev)
+    xs = synth.make_trajectory(wl, logp)
+    ms = timed(lambda: D.dbl_acceptance_objective(tls, lmass, lse, ell, xs, logp, z_temp=wl.z_temp))
+    rows["acceptance_objective"] = {"ms": ms, "bound": "latency", "blocks": B}
+    del tls, lmass, lse, h
+    # Target transform on the verification rows (K + 1 per block) with the paper's filters.
+    g = synth.make_target_logits(wl, K + 1, device=dev).to(torch.float32)
+    lp = torch.empty_like(g)
+    nbytes = 2.0 * g.numel() * 4
+    for T, k, p in ((0.7, 20, 0.8), (1.0, 20, 0.95), (1.0, 0, 0.95)):
+        ms = timed(lambda: D.dbl_target_logprobs(g, T, k, p, out=lp))
+        rows[f"target_logprobs_T{T}_k{k}_p{p}"] = hbm(ms, nbytes)
+    # Early determinism on the filtered rows.
+    rng = np.random.default_rng(0)
+    xd = torch.from_numpy(rng.integers(0, V, size=(B, K + 1), dtype=np.int32)).to(dev)
+    ms = timed(lambda: D.dbl_early_determinism(xd, lp))
+    rows["early_determinism"] = {"ms": ms, "bound": "latency", "blocks": B}
+    return {"metric": "per-call time of the entry points outside the step", "rows": rows,
+            "steps": steps, "warmup": warmup, "data": "synthetic",
+            "config": {"workload": wl.name, "B": B, "K": K, "R": R, "d": d, "V": V,
+                       "target_rows": B * (K + 1)}}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -155,7 +233,7 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3_8b")
     ap.add_argument("--temperature", type=float, default=None)
-    ap.add_argument("--mode", choices=("soft", "greedy"), default="soft")
+    ap.add_argument("--mode", choices=("soft", "greedy", "rows"), default="soft")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", type=int, default=0)
@@ -195,6 +273,9 @@ def main(argv=None):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     D.load()
+    if args.mode == "rows":
+        print(json.dumps(_rows(wl, dev, args.steps, args.warmup)), flush=True)
+        return 0
 
     # Inputs resident in HBM before timing.
     h = synth.make_h(wl, dev)

@@ -868,20 +868,33 @@ __global__ __launch_bounds__(256) void prior_head_kernel(const __bf16* __restric
 
 }  // namespace
 
-hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {
-  const int64_t N = a.R * a.d;
-  const int dm = static_cast<int>((a.M + DCfg::BM - 1) / DCfg::BM);
-  const int64_t dwg = ((N + DCfg::BV - 1) / DCfg::BV) * dm;
-  if (dwg > 0x7fffffff || a.d % DCfg::BK != 0) return hipErrorInvalidConfiguration;
+// Expander GEMMs have few trunk rows (B*K) and a wide output (R*d): when 256-row tiles would not
+// give every CU a workgroup, 128-row tiles double the workgroup count (the weight slab each
+// pair of them shares is read from L2).
+using ECfg = DmaCfg<32, 4, 128, 2>;
+constexpr int kCus = 256;
+
+template <class C>
+hipError_t launch_expand_cfg(const ExpandArgs& a, int64_t N, hipStream_t stream) {
+  const int dm = static_cast<int>((a.M + C::BM - 1) / C::BM);
+  const int64_t dwg = ((N + C::BV - 1) / C::BV) * dm;
+  if (dwg > 0x7fffffff || a.d % C::BK != 0) return hipErrorInvalidConfiguration;
   EpiArgs ea{};
   ea.out = static_cast<__bf16*>(a.out);
   ea.bias = static_cast<const __bf16*>(a.c);
   ea.hres = static_cast<const __bf16*>(a.h);
   ea.dres = a.d;
-  hipLaunchKernelGGL((head_bf16_dma_kernel<DCfg, kEpiExpand>), dim3(static_cast<unsigned>(dwg)),
-                     dim3(DCfg::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
+  hipLaunchKernelGGL((head_bf16_dma_kernel<C, kEpiExpand>), dim3(static_cast<unsigned>(dwg)),
+                     dim3(C::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
                      static_cast<const __bf16*>(a.W), ea, a.M, N, a.d, dm);
   return hipGetLastError();
+}
+
+hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {
+  const int64_t N = a.R * a.d;
+  const int64_t wg256 = ((N + DCfg::BV - 1) / DCfg::BV) * ((a.M + DCfg::BM - 1) / DCfg::BM);
+  if (wg256 < kCus) return launch_expand_cfg<ECfg>(a, N, stream);
+  return launch_expand_cfg<DCfg>(a, N, stream);
 }
 
 hipError_t launch_prior_head(const PriorHeadArgs& a, hipStream_t stream) {

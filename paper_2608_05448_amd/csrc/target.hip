@@ -151,30 +151,49 @@ __device__ __forceinline__ uint64_t visit_key(uint32_t key, int64_t v) {
   return (static_cast<uint64_t>(key) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(v));
 }
 
-// Fast path for top-k (0 < k <= kFastK < V): three streaming passes over the row instead of up
-// to ten, none of which divides more than a few candidates (fl32(x / T) is monotone in x, so
-// selections on s can be made on the logits' keys):
-//   1. every thread keeps the four largest logit keys it sees; the k-th largest t of these 4096
-//      keys (found by bisection) is at most the row's k-th largest, the union being part of
-//      the row, so s_t = fl32(t / T) is at most the k-th largest s;
-//   2. every token with s >= s_t (logit key at least least_logit_key(s_t)) is appended to an
-//      LDS list with its s;
-//   3. the list is sorted in visiting order; both cuts and the normaliser follow from it, and a
-//      token is kept iff its visiting key is at least that of the last kept token;
-//   4. the output row is written; only logits at or above the cut's least key are divided.
-// Returns false (the caller then runs the radix path) if the list would overflow LDS.
+// k-th largest of the 64 x 4 keys held by a wavefront (k <= 256): the largest t with at least k
+// of them >= t, by bisection with ballots; no LDS, no barrier.
+__device__ __forceinline__ uint32_t wave_kth_largest(uint32_t t0, uint32_t t1, uint32_t t2,
+                                                     uint32_t t3, int k) {
+  uint64_t lo = 0, hi = 0xFFFFFFFFu;  // count(>= lo) >= k always (every key is >= 0)
+  while (lo < hi) {
+    const uint64_t mid = lo + (hi - lo + 1) / 2;
+    const uint32_t m32 = static_cast<uint32_t>(mid);
+    const int c = __popcll(__ballot(t0 >= m32)) + __popcll(__ballot(t1 >= m32)) +
+                  __popcll(__ballot(t2 >= m32)) + __popcll(__ballot(t3 >= m32));
+    if (c >= k) lo = mid; else hi = mid - 1;
+  }
+  return static_cast<uint32_t>(lo);
+}
+
+// Fast path for top-k (0 < k <= kFastK < V): one streaming read and one streaming write of the
+// row (fl32(x / T) is monotone in x, so selections on s are made on the logits' keys and only
+// candidates are divided):
+//   1. every thread writes -inf over its part of the output row and keeps the four largest logit
+//      keys it sees;
+//   2. a lower bound t of the row's k-th largest key: the largest over wavefronts of each
+//      wavefront's k-th largest held key (k <= 256), else the k-th largest of all 4096 held keys
+//      (workgroup bisection); each is the k-th largest of part of the row;
+//   3. only threads holding a key >= x_low = least_logit_key(fl32(t / T)) can own a token with
+//      s >= fl32(t / T) (their other logits are below their fourth largest); they re-read their
+//      own ids and append every such token, with its s, to an LDS list;
+//   4. the list is sorted in visiting order (s descending, id ascending); both cuts and the
+//      normaliser follow from it, and the kept tokens' log-probabilities overwrite the -inf.
+// Returns false (the caller then runs the radix path, which rewrites the whole row) if the list
+// would overflow LDS.
 constexpr int kFastK = 1024;
 constexpr int kCandCap = 4096;
 
 __device__ bool filter_fast(const FilterArgs& a, const float* in, float* out, bool vec,
-                            uint64_t* cand, uint64_t* red, double* redd, int* sh_n) {
+                            uint64_t* cand, int* resc, uint64_t* red, double* redd, int* sh_n,
+                            int* sh_r) {
   const int tid = threadIdx.x;
   const int64_t V = a.V;
   const float T = a.temperature;
   const int k = static_cast<int>(a.top_k);
-  // 1. per-thread top-4 logit keys
+  // 1. -inf over the row; per-thread top-4 logit keys
   uint32_t t0 = 0, t1 = 0, t2 = 0, t3 = 0;
-  row_scan_raw(in, V, vec, [&](int64_t, float lv) {
+  auto insert = [&](float lv) {
     uint32_t x = order_key(lv);  // insertion into t0 >= t1 >= t2 >= t3, branch-free
     uint32_t y = max(t0, x);
     x = min(t0, x);
@@ -186,39 +205,120 @@ __device__ bool filter_fast(const FilterArgs& a, const float* in, float* out, bo
     x = min(t2, x);
     t2 = y;
     t3 = max(t3, x);
-  });
-  // k-th largest of the union: largest t with at least k union entries >= t (t = 0 always has
-  // all 4096, and 4096 >= k).
-  uint64_t lo = 0, hi = block_max_u64(t0, red);
-  while (lo < hi) {
-    const uint64_t mid = lo + (hi - lo + 1) / 2;
-    const uint32_t m32 = static_cast<uint32_t>(mid);
-    const uint32_t c = __popcll(__ballot(t0 >= m32)) + __popcll(__ballot(t1 >= m32)) +
-                       __popcll(__ballot(t2 >= m32)) + __popcll(__ballot(t3 >= m32));
-    if (lane_id() == 0) red[tid >> 6] = c;
-    __syncthreads();
-    uint64_t tot = 0;
+  };
+  if (vec) {
+    const float4* in4 = reinterpret_cast<const float4*>(in);
+    float4* out4 = reinterpret_cast<float4*>(out);
+    const int64_t n4 = V >> 2;
+    const float4 ninf = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    int64_t j = tid;
+    for (; j + (kBatch - 1) * kFT < n4; j += kBatch * kFT) {
+      float4 x[kBatch];
 #pragma unroll
-    for (int w = 0; w < kFW; ++w) tot += red[w];
-    __syncthreads();
-    if (tot >= static_cast<uint64_t>(k)) lo = mid; else hi = mid - 1;
+      for (int u = 0; u < kBatch; ++u) x[u] = in4[j + u * kFT];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        out4[j + u * kFT] = ninf;
+        insert(x[u].x);
+        insert(x[u].y);
+        insert(x[u].z);
+        insert(x[u].w);
+      }
+    }
+    for (; j < n4; j += kFT) {
+      const float4 x = in4[j];
+      out4[j] = ninf;
+      insert(x.x);
+      insert(x.y);
+      insert(x.z);
+      insert(x.w);
+    }
+  } else {
+    for (int64_t v = tid; v < V; v += kFT) {
+      insert(in[v]);
+      out[v] = -INFINITY;
+    }
   }
-  const uint32_t s_low = order_key(__fdiv_rn(key_value(static_cast<uint32_t>(lo)), T));
+  // The kept tokens' values are stored later, possibly by other threads, over these -inf: wait
+  // for this thread's stores before the barriers that follow.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // 2. lower bound of the row's k-th largest logit key
+  uint32_t tlow;
+  if (k <= 256) {
+    tlow = static_cast<uint32_t>(block_max_u64(wave_kth_largest(t0, t1, t2, t3, k), red));
+  } else {
+    uint64_t lo = 0, hi = block_max_u64(t0, red);
+    while (lo < hi) {
+      const uint64_t mid = lo + (hi - lo + 1) / 2;
+      const uint32_t m32 = static_cast<uint32_t>(mid);
+      const uint32_t c = __popcll(__ballot(t0 >= m32)) + __popcll(__ballot(t1 >= m32)) +
+                         __popcll(__ballot(t2 >= m32)) + __popcll(__ballot(t3 >= m32));
+      if (lane_id() == 0) red[tid >> 6] = c;
+      __syncthreads();
+      uint64_t tot = 0;
+#pragma unroll
+      for (int w = 0; w < kFW; ++w) tot += red[w];
+      __syncthreads();
+      if (tot >= static_cast<uint64_t>(k)) lo = mid; else hi = mid - 1;
+    }
+    tlow = static_cast<uint32_t>(lo);
+  }
+  const uint32_t s_low = order_key(__fdiv_rn(key_value(tlow), T));
   const uint32_t x_low = least_logit_key(s_low, T);
-  // 2. append every token with s >= s_t
-  if (tid == 0) *sh_n = 0;
+  // 3. candidates from the threads that hold a key >= x_low: their ids are re-read by the whole
+  //    workgroup (item w = (listed thread w / G, its w % G-th load), G loads per thread)
+  if (tid == 0) {
+    *sh_n = 0;
+    *sh_r = 0;
+  }
   __syncthreads();
-  row_scan_raw(in, V, vec, [&](int64_t v, float lv) {
+  if (t0 >= x_low) resc[atomicAdd(sh_r, 1)] = tid;
+  __syncthreads();
+  const int nr = *sh_r;
+  const int64_t units = vec ? (V >> 2) : V;              // float4 groups or single ids
+  const int G = static_cast<int>((units + kFT - 1) / kFT);  // loads per thread, at most
+  const int64_t items = static_cast<int64_t>(nr) * G;
+  auto take = [&](int64_t v, float lv) {
     if (order_key(lv) >= x_low) {
       const int slot = atomicAdd(sh_n, 1);
       if (slot < kCandCap) cand[slot] = visit_key(order_key(__fdiv_rn(lv, T)), v);
     }
-  });
+  };
+  for (int64_t w0 = tid; w0 < items; w0 += kBatch * kFT) {
+    int64_t jj[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int64_t w = w0 + static_cast<int64_t>(b) * kFT;
+      const int64_t j = w < items ? resc[w / G] + (w % G) * static_cast<int64_t>(kFT) : units;
+      jj[b] = j < units ? j : -1;
+    }
+    if (vec) {
+      const float4* in4 = reinterpret_cast<const float4*>(in);
+      float4 x[kBatch];
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) x[b] = jj[b] >= 0 ? in4[jj[b]] : make_float4(0, 0, 0, 0);
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) {
+        if (jj[b] < 0) continue;
+        take(4 * jj[b], x[b].x);
+        take(4 * jj[b] + 1, x[b].y);
+        take(4 * jj[b] + 2, x[b].z);
+        take(4 * jj[b] + 3, x[b].w);
+      }
+    } else {
+      float x[kBatch];
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) x[b] = jj[b] >= 0 ? in[jj[b]] : 0.0f;
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b)
+        if (jj[b] >= 0) take(jj[b], x[b]);
+    }
+  }
   __syncthreads();
   const int n = *sh_n;
   __syncthreads();
   if (n > kCandCap) return false;
-  // 3. bitonic sort, descending, of the list padded with zeros to a power of two (every real
+  // 4. bitonic sort, descending, of the list padded with zeros to a power of two (every real
   //    entry has a nonzero low word, ids being below 2^32 - 1)
   int np = 64;
   while (np < n) np <<= 1;
@@ -282,43 +382,16 @@ __device__ bool filter_fast(const FilterArgs& a, const float* in, float* out, bo
     }
     nkeep = static_cast<int>(block_sum_u64(c, red));
   }
-  const uint64_t cut = cand[nkeep - 1];
   double se = 0.0;
   for (int i = tid; i < nkeep; i += kFT)
     se += exp(static_cast<double>(key_value(key_at(i))) - static_cast<double>(m));
   const double lse = log(block_sum_f64(se, redd));
-  // 4. output row
-  const uint32_t x_cut = least_logit_key(static_cast<uint32_t>(cut >> 32), T);
-  auto val = [&](int64_t v, float lv) {
-    if (order_key(lv) < x_cut) return -INFINITY;
-    const float sv = __fdiv_rn(lv, T);
-    return visit_key(order_key(sv), v) >= cut
-               ? static_cast<float>(static_cast<double>(sv) - static_cast<double>(m) - lse)
-               : -INFINITY;
-  };
-  if (vec) {
-    const float4* in4 = reinterpret_cast<const float4*>(in);
-    float4* out4 = reinterpret_cast<float4*>(out);
-    const int64_t n4 = V >> 2;
-    auto one = [&](int64_t j, const float4& x) {
-      float4 y;
-      y.x = val(4 * j, x.x);
-      y.y = val(4 * j + 1, x.y);
-      y.z = val(4 * j + 2, x.z);
-      y.w = val(4 * j + 3, x.w);
-      out4[j] = y;
-    };
-    int64_t j = tid;
-    for (; j + (kBatch - 1) * kFT < n4; j += kBatch * kFT) {
-      float4 x[kBatch];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) x[u] = in4[j + u * kFT];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) one(j + u * kFT, x[u]);
-    }
-    for (; j < n4; j += kFT) one(j, in4[j]);
-  } else {
-    for (int64_t v = tid; v < V; v += kFT) out[v] = val(v, in[v]);
+  // 5. kept tokens (the first nkeep entries of the list)
+  for (int i = tid; i < nkeep; i += kFT) {
+    const uint64_t e = cand[i];
+    const int64_t v = 0xFFFFFFFFu - static_cast<uint32_t>(e);
+    out[v] = static_cast<float>(static_cast<double>(key_value(static_cast<uint32_t>(e >> 32))) -
+                                static_cast<double>(m) - lse);
   }
   return true;
 }
@@ -326,7 +399,8 @@ __device__ bool filter_fast(const FilterArgs& a, const float* in, float* out, bo
 __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
   __shared__ uint64_t hist[256];
   __shared__ uint64_t cand[kCandCap];
-  __shared__ int sh_n;
+  __shared__ int resc[kFT];
+  __shared__ int sh_n, sh_r;
   __shared__ uint64_t red[kFW];
   __shared__ double redd[kFW];
   __shared__ uint32_t sh_digit;
@@ -354,7 +428,7 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
   const bool vec = (V & 3) == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(out) & 15) == 0;
   if (a.top_k > 0 && a.top_k <= kFastK && a.top_k < V &&
-      filter_fast(a, in, out, vec, cand, red, redd, &sh_n))
+      filter_fast(a, in, out, vec, cand, resc, red, redd, &sh_n, &sh_r))
     return;
 
   // Row maximum (key of the largest s).
