@@ -13,6 +13,8 @@ argmax, then dbl_sample_greedy and dbl_verify_greedy.
 With --mode rows the line instead times the other entry points at the workload's shape (branch
 expander, prior head, objective forward, target transform, early-determinism estimate), each
 against its own bound; it is a measurement aid, not the step metric.
+With --workload objective (2048 blocks, R = 16) a step runs every 128-block chunk through the
+head, dbl_expected_len and dbl_acceptance_objective.
 
 The metric is verified block positions per second, B*K / step time. The roofline entry is for
 the dominant kernel, the head GEMM: 2*M*d*V flops per launch over its average launch time,
@@ -226,6 +228,91 @@ def _rows(wl, dev, steps: int, warmup: int):
                        "target_rows": B * (K + 1)}}
 
 
+def _objective_chunks(wl, dev, steps: int, warmup: int, chunk: int = 128):
+    """The training-objective workload (2048 blocks, R = 16): one step runs every chunk of
+    `chunk` blocks through dbl_head_logprobs, dbl_expected_len (β and E along the target
+    trajectory) and dbl_acceptance_objective, with all chunks' inputs resident in HBM."""
+    import torch
+
+    import synth
+    from paper_2608_05448_amd import dblast as D
+
+    B, K, R, d, V = wl.B, wl.K, wl.R, wl.d, wl.V
+    nT = D.ntiles(V)
+    w = synth.make_w(wl, dev)
+    ell = synth.make_ell(wl, dev)
+    chunks = []
+    for c0 in range(0, B, chunk):
+        blocks = range(c0, min(B, c0 + chunk))
+        lp = synth.make_logp(wl, rows=K, device=dev, blocks=blocks)
+        chunks.append((synth.make_h(wl, dev, blocks=blocks), lp, synth.make_trajectory(wl, lp, blocks),
+                       ell[c0:c0 + len(blocks)].contiguous()))
+    nb = len(chunks[0][2])
+    tls = torch.empty((nb, K, R, V), dtype=torch.float32, device=dev)
+    lmass = torch.empty((nb, K, R, nT), dtype=torch.float32, device=dev)
+    lse = torch.empty((nb, K, R), dtype=torch.float32, device=dev)
+    beta = torch.empty((nb, K), dtype=torch.float32, device=dev)
+    e = torch.empty(nb, dtype=torch.float32, device=dev)
+    ws = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_EXPECTED_LEN, nb, K, R, d, V),
+                     dtype=torch.uint8, device=dev)
+    obj = {k: torch.empty(nb, dtype=t, device=dev)
+           for k, t in (("ell_tau", torch.int32), ("J", torch.float32), ("nll", torch.float32))}
+    stream = torch.cuda.current_stream(dev)
+    ev = []
+
+    def step(record):
+        for h, lp, xs, el in chunks:
+            if len(xs) != nb:
+                raise ValueError("the block count must be a multiple of the chunk size")
+            e0, e1, e2, e3 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
+            if record:
+                e0.record(stream)
+            D.dbl_head_logprobs(h, w, tls, lmass, lse)
+            if record:
+                e1.record(stream)
+            D.dbl_expected_len(tls, lmass, lse, el, xs, lp, z_temp=wl.z_temp, beta=beta,
+                               exp_len=e, ws=ws)
+            if record:
+                e2.record(stream)
+            D.dbl_acceptance_objective(tls, lmass, lse, el, xs, lp, z_temp=wl.z_temp, tau=0.1,
+                                       want_terms=False, out=obj)
+            if record:
+                e3.record(stream)
+                ev.append((e0, e1, e2, e3))
+
+    for _ in range(warmup):
+        step(False)
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step(True)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    n = len(ev)
+    head_ms = sum(a.elapsed_time(b) for a, b, _, _ in ev) / n
+    el_ms = sum(b.elapsed_time(c) for _, b, c, _ in ev) / n
+    ob_ms = sum(c.elapsed_time(d_) for _, _, c, d_ in ev) / n
+    step_ms = ev[0][0].elapsed_time(ev[-1][3]) / steps
+    M = nb * K * R
+    head_tflops = 2.0 * M * d * V / (head_ms * 1e-3) / 1e12
+    el_bytes = nb * K * (R + 1) * V * 4.0
+    return {"metric": "positions/s of head + expected length + objective forward",
+            "value": B * K / (step_ms * 1e-3), "unit": "positions/s", "n_gpus": 1,
+            "steps": steps, "warmup": warmup, "ms_per_step": step_ms, "higher_is_better": True,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": wl.name, "B": B, "K": K, "R": R, "d": d, "V": V,
+                       "chunk_blocks": nb, "chunks": len(chunks)},
+            "per_chunk_ms": {"head": head_ms, "expected_len": el_ms, "objective": ob_ms},
+            "roofline": {"bound": "mfma", "achieved": head_tflops, "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": head_tflops / PEAK_BF16_TFLOPS,
+                         "kernel": "dbl_head_logprobs"},
+            "hbm": {"expected_len_GBps": el_bytes / (el_ms * 1e-3) / 1e9,
+                    "expected_len_frac": el_bytes / (el_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
+            "quality": {"mean_exp_len_last_chunk": float(e.mean().item()),
+                        "mean_J_last_chunk": float(obj["J"].mean().item())},
+            "wall_s_timed": wall}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -275,6 +362,9 @@ def main(argv=None):
     D.load()
     if args.mode == "rows":
         print(json.dumps(_rows(wl, dev, args.steps, args.warmup)), flush=True)
+        return 0
+    if wl.name == "objective":
+        print(json.dumps(_objective_chunks(wl, dev, args.steps, args.warmup)), flush=True)
         return 0
 
     # Inputs resident in HBM before timing.
@@ -349,6 +439,8 @@ def main(argv=None):
     sample_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps
     verify_ms = sum(e[2].elapsed_time(e[3]) for e in events) / args.steps
     step_ms = events[0][0].elapsed_time(events[-1][3]) / args.steps
+    per_step = sorted(e[0].elapsed_time(e[3]) for e in events)
+    pct = {q: per_step[min(len(per_step) - 1, int(q / 100 * len(per_step)))] for q in (10, 50, 90)}
     acc_sum = float(vout["n_accept"].float().mean().item())
     exp_len = float(vout["exp_len"].float().mean().item())
 
@@ -384,6 +476,7 @@ def main(argv=None):
                      "traffic": traffic,
                      "kernel": "dbl_head_logprobs (head GEMM + per-tile log-softmax, LSE)"},
         "kernels_ms": {"head": head_ms, "sample": sample_ms, "verify": verify_ms},
+        "step_ms_p10_p50_p90": [pct[10], pct[50], pct[90]],
         "hbm": {"verify_GBps": verify_bytes / (verify_ms * 1e-3) / 1e9,
                 "verify_frac": verify_bytes / (verify_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
                 "sample_GBps": sample_bytes / (sample_ms * 1e-3) / 1e9,
