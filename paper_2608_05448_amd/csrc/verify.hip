@@ -167,9 +167,9 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
 constexpr float kLog2eF = 1.4426950408889634f;
 
 template <int RT>
-__global__ __launch_bounds__(256) void beta_kernel(VerifyArgs a) {
+__device__ __forceinline__ void beta_body(const VerifyArgs& a, int64_t pos, int chunk,
+                                          int nchunk) {
   const BlockArgs& k_ = a.blk;
-  const int64_t pos = blockIdx.x;
   const int64_t b = pos / k_.K;
   const int64_t k = pos % k_.K;
   const int R = RT > 0 ? RT : static_cast<int>(k_.R);
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(256) void beta_kernel(VerifyArgs a) {
   __shared__ float s_w[kMaxR];
   __shared__ float s_off[kMaxR][kTilesPerChunk];
   __shared__ float red[4];
-  const int t0 = blockIdx.y * kTilesPerChunk;
+  const int t0 = chunk * kTilesPerChunk;
   const int nt = min(kTilesPerChunk, k_.nT - t0);
   const int64_t m0 = pos * k_.R;
   for (int i = threadIdx.x; i < R * kTilesPerChunk; i += blockDim.x) {
@@ -237,7 +237,12 @@ __global__ __launch_bounds__(256) void beta_kernel(VerifyArgs a) {
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
   __syncthreads();
   if (threadIdx.x == 0)
-    a.beta_part[pos * gridDim.y + blockIdx.y] = (red[0] + red[1]) + (red[2] + red[3]);
+    a.beta_part[pos * nchunk + chunk] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+template <int RT>
+__global__ __launch_bounds__(256) void beta_kernel(VerifyArgs a) {
+  beta_body<RT>(a, blockIdx.x, blockIdx.y, gridDim.y);
 }
 
 // Integer weight of id v in the residual / bonus distributions.
@@ -272,9 +277,8 @@ struct ResidualWeight {
 // Q(v) = floor((sum over ascending z of w_z detexp32(lq_z(v))) 2^40); after full acceptance
 // only P of the bonus row. RT > 0 fixes the number of categories at compile time.
 template <int RT>
-__global__ __launch_bounds__(256) void residual_kernel(VerifyArgs a) {
+__device__ __forceinline__ void residual_body(const VerifyArgs& a, int64_t b, int chunk) {
   const BlockArgs& k_ = a.blk;
-  const int64_t b = blockIdx.x;
   const int ks = a.n_accept[b];
   const bool residual = ks < k_.K;
   if (!residual && a.Kp != k_.K + 1) return;
@@ -283,7 +287,7 @@ __global__ __launch_bounds__(256) void residual_kernel(VerifyArgs a) {
   if (residual && threadIdx.x < R) wz[threadIdx.x] = a.wpost[(b * k_.K + ks) * k_.R + threadIdx.x];
   __syncthreads();
   const int sub = threadIdx.x & 7;
-  const int t = blockIdx.y * kTilesPerChunk + (threadIdx.x >> 3);
+  const int t = chunk * kTilesPerChunk + (threadIdx.x >> 3);
   const int64_t V = k_.V;
   uint64_t sp = 0, sr = 0;
   if (t < k_.nT) {
@@ -326,6 +330,7 @@ __global__ __launch_bounds__(256) void residual_kernel(VerifyArgs a) {
         const int v = 4 * sub + 32 * i;
         if (v0 + v < V) {
           const float4 p4 = *reinterpret_cast<const float4*>(prow + v);
+          const float pe[4] = {p4.x, p4.y, p4.z, p4.w};
           float4 x4[RT > 0 ? RT : 1];
           if constexpr (RT > 0) {
             if (residual) {
@@ -333,12 +338,9 @@ __global__ __launch_bounds__(256) void residual_kernel(VerifyArgs a) {
               for (int z = 0; z < RT; ++z)
                 x4[z] = *reinterpret_cast<const float4*>(trow + z * V + v);
             }
-          }
-          const float pe[4] = {p4.x, p4.y, p4.z, p4.w};
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            uint64_t P, Rw;
-            if constexpr (RT > 0) {
+            for (int e = 0; e < 4; ++e) {
+              uint64_t P, Rw;
               float tv[RT];
               if (residual) {
 #pragma unroll
@@ -346,11 +348,17 @@ __global__ __launch_bounds__(256) void residual_kernel(VerifyArgs a) {
                   tv[z] = e == 0 ? x4[z].x : e == 1 ? x4[z].y : e == 2 ? x4[z].z : x4[z].w;
               }
               weights(v + e, pe[e], tv, 1, P, Rw);
-            } else {
-              weights(v + e, pe[e], trow + v + e, static_cast<int>(V), P, Rw);
+              sp += P;
+              sr += Rw;
             }
-            sp += P;
-            sr += Rw;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              uint64_t P, Rw;
+              weights(v + e, pe[e], trow + v + e, static_cast<int>(V), P, Rw);
+              sp += P;
+              sr += Rw;
+            }
           }
         }
       }
@@ -385,6 +393,23 @@ __global__ __launch_bounds__(256) void residual_kernel(VerifyArgs a) {
     a.p_tiles[b * k_.nT + t] = sp;
     a.res_tiles[b * k_.nT + t] = sr;
   }
+}
+
+template <int RT>
+__global__ __launch_bounds__(256) void residual_kernel(VerifyArgs a) {
+  residual_body<RT>(a, blockIdx.x, blockIdx.y);
+}
+
+// Residual / bonus tile sums and the acceptance-mass stream in one launch: workgroups
+// x < B are the residual's (issued first, so its ALU-heavy blocks overlap the stream), the rest
+// the acceptance-mass stream's. The two write disjoint outputs.
+template <int RT>
+__global__ __launch_bounds__(256) void beta_residual_kernel(VerifyArgs a) {
+  const int64_t B = a.blk.B;
+  if (blockIdx.x < B)
+    residual_body<RT>(a, blockIdx.x, blockIdx.y);
+  else
+    beta_body<RT>(a, blockIdx.x - B, blockIdx.y, gridDim.y);
 }
 
 // Per block: acceptance masses and E (binary64 sums of the chunk partials), then the residual
@@ -464,7 +489,19 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const bool want_beta = a.beta || a.exp_len;
-  if (want_beta) {
+  if (want_beta && !a.trajectory) {
+    if (npos + B > 0x7fffffff) return hipErrorInvalidConfiguration;
+    const dim3 grid(static_cast<unsigned>(B + npos), nchunk);
+    switch (a.blk.R) {
+      case 1: hipLaunchKernelGGL(beta_residual_kernel<1>, grid, dim3(256), 0, stream, a); break;
+      case 2: hipLaunchKernelGGL(beta_residual_kernel<2>, grid, dim3(256), 0, stream, a); break;
+      case 4: hipLaunchKernelGGL(beta_residual_kernel<4>, grid, dim3(256), 0, stream, a); break;
+      case 8: hipLaunchKernelGGL(beta_residual_kernel<8>, grid, dim3(256), 0, stream, a); break;
+      case 16: hipLaunchKernelGGL(beta_residual_kernel<16>, grid, dim3(256), 0, stream, a); break;
+      default: hipLaunchKernelGGL(beta_residual_kernel<0>, grid, dim3(256), 0, stream, a); break;
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else if (want_beta) {
     const dim3 grid(static_cast<unsigned>(npos), nchunk);
     switch (a.blk.R) {
       case 1: hipLaunchKernelGGL(beta_kernel<1>, grid, dim3(256), 0, stream, a); break;
@@ -475,8 +512,7 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
       default: hipLaunchKernelGGL(beta_kernel<0>, grid, dim3(256), 0, stream, a); break;
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
-  if (!a.trajectory) {
+  } else if (!a.trajectory) {
     const dim3 grid(static_cast<unsigned>(B), nchunk);
     switch (a.blk.R) {
       case 1: hipLaunchKernelGGL(residual_kernel<1>, grid, dim3(256), 0, stream, a); break;
