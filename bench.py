@@ -222,6 +222,16 @@ def _rows(wl, dev, steps: int, warmup: int):
     xd = torch.from_numpy(rng.integers(0, V, size=(B, K + 1), dtype=np.int32)).to(dev)
     ms = timed(lambda: D.dbl_early_determinism(xd, lp))
     rows["early_determinism"] = {"ms": ms, "bound": "latency", "blocks": B}
+    # Reference rates for the streaming kernels, over as many bytes as the verify stream reads:
+    # the library's plain streaming-read probe and a plain device copy.
+    del g, lp
+    buf = torch.empty(B * K * (R + 1) * V, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(buf)
+    parts = torch.empty(2048, dtype=torch.float32, device=dev)
+    ms = timed(lambda: D.dbl_stream_read_probe(buf, parts))
+    rows["reference_read"] = hbm(ms, buf.numel() * 4.0)
+    ms = timed(lambda: dst.copy_(buf))
+    rows["reference_copy"] = hbm(ms, buf.numel() * 8.0)
     return {"metric": "per-call time of the entry points outside the step", "rows": rows,
             "steps": steps, "warmup": warmup, "data": "synthetic",
             "config": {"workload": wl.name, "B": B, "K": K, "R": R, "d": d, "V": V,

@@ -351,6 +351,18 @@ dbl_status dbl_target_logprobs(int64_t N, int64_t V, const float* logits, float 
 dbl_status dbl_early_determinism(int64_t M, int64_t b, int64_t V, const int32_t* x,
                                  const float* logp, float* terms, float* mean, void* stream);
 
+/*
+ * dbl_stream_read_probe - a diagnostic, not an operation of the method: reads every 16-byte
+ * word of buf once (float4 loads, n_partials workgroups of 256 threads striding over the
+ * buffer) and writes each workgroup's sum of the values it read to partials[i]. Its time gives
+ * the plain streaming-read rate against which the bandwidth-bound kernels are judged.
+ *   buf      device, 16-byte aligned, `bytes` bytes (a multiple of 16), read as fp32
+ *   partials device, [n_partials] fp32 out;  1 <= n_partials <= 2^20
+ * Errors: DBL_EINVAL for null or misaligned pointers; DBL_ESHAPE for sizes.
+ */
+dbl_status dbl_stream_read_probe(const void* buf, int64_t bytes, float* partials,
+                                 int64_t n_partials, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -28,6 +28,7 @@ SOURCES = {
     "greedy.hip": ["-ffp-contract=off"],
     "objective.hip": [],
     "target.hip": ["-ffp-contract=off"],
+    "diag.hip": [],
 }
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

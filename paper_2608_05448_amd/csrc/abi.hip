@@ -465,4 +465,16 @@ dbl_status dbl_early_determinism(int64_t M, int64_t b, int64_t V, const int32_t*
                     "early determinism launch");
 }
 
+dbl_status dbl_stream_read_probe(const void* buf, int64_t bytes, float* partials,
+                                 int64_t n_partials, void* stream) {
+  if (!buf || !partials) return fail(DBL_EINVAL, "NULL pointer");
+  if (bytes < 0 || bytes % 16 != 0) return fail(DBL_ESHAPE, "bytes must be a multiple of 16");
+  if (n_partials < 1 || n_partials > (int64_t(1) << 20))
+    return fail(DBL_ESHAPE, "need 1 <= n_partials <= 2^20");
+  if (reinterpret_cast<uintptr_t>(buf) % 16 != 0) return fail(DBL_EINVAL, "buf not 16-byte aligned");
+  return hip_status(dbl::launch_read_probe(buf, bytes, partials, n_partials,
+                                           static_cast<hipStream_t>(stream)),
+                    "read probe launch");
+}
+
 }  // extern "C"

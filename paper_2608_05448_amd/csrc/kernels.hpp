@@ -145,5 +145,7 @@ hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream);
 hipError_t launch_prior_head(const PriorHeadArgs& a, hipStream_t stream);
 hipError_t launch_filter(const FilterArgs& a, hipStream_t stream);
 hipError_t launch_determinism(const DeterminismArgs& a, hipStream_t stream);
+hipError_t launch_read_probe(const void* buf, int64_t bytes, float* partials, int64_t n_partials,
+                             hipStream_t stream);
 
 }  // namespace dbl

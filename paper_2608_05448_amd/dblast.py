@@ -63,6 +63,7 @@ _SIGS = {
     "dbl_prior_head": (ctypes.c_int, [Shape, _P, _P, _P, _P, _P]),
     "dbl_target_logprobs": (ctypes.c_int, [_I64, _I64, _P, _F, _I64, _F, _P, _P]),
     "dbl_early_determinism": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P]),
+    "dbl_stream_read_probe": (ctypes.c_int, [_P, _I64, _P, _I64, _P]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -398,3 +399,14 @@ def dbl_early_determinism(x, logp):
     _check(load().dbl_early_determinism(M, b, logp.shape[-1], _ptr(x), _ptr(logp), _ptr(terms),
                                         _ptr(mean), _stream(dev)))
     return terms, mean
+
+
+def dbl_stream_read_probe(buf, partials):
+    """Diagnostic: read every 16-byte word of ``buf`` once (one workgroup per element of
+    ``partials``, fp32 [n]); each writes the sum of the values it read. Returns ``partials``."""
+    _need(buf, "buf", buf.dtype)
+    _need(partials, "partials", torch.float32)
+    nbytes = buf.numel() * buf.element_size()
+    _check(load().dbl_stream_read_probe(_ptr(buf), nbytes, _ptr(partials), partials.numel(),
+                                        _stream(buf.device)))
+    return partials

@@ -203,3 +203,16 @@ def test_objective_validation(lib):
     assert lib.dbl_acceptance_objective(S(0, 4, 3, 0, 300), p[0], p[1], p[2], p[3], 1.0, p[4],
                                         p[5], 0.1, null, null, p[6], p[7], p[8],
                                         null) == D.DBL_OK
+
+
+def test_read_probe_validation(lib):
+    p = _fake(2)
+    null = ctypes.c_void_p(None)
+    assert lib.dbl_stream_read_probe(null, 64, p[1], 4, null) == D.DBL_EINVAL
+    assert lib.dbl_stream_read_probe(p[0], 64, null, 4, null) == D.DBL_EINVAL
+    assert lib.dbl_stream_read_probe(p[0], 60, p[1], 4, null) == D.DBL_ESHAPE
+    assert lib.dbl_stream_read_probe(p[0], -16, p[1], 4, null) == D.DBL_ESHAPE
+    assert lib.dbl_stream_read_probe(p[0], 64, p[1], 0, null) == D.DBL_ESHAPE
+    assert lib.dbl_stream_read_probe(p[0], 64, p[1], (1 << 20) + 1, null) == D.DBL_ESHAPE
+    assert lib.dbl_stream_read_probe(ctypes.c_void_p(p[0].value + 4), 64, p[1], 4,
+                                     null) == D.DBL_EINVAL
