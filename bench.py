@@ -153,11 +153,14 @@ def _copy_calibration(nbytes: int):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 3}))
 
 
-def _rows(wl, dev, steps: int, warmup: int):
+def _rows(wl, dev, steps: int, warmup: int, cpu: bool = True):
     """Average time per call (HIP events on the library's stream) of the entry points outside
-    the step, at the workload's shape, each with its algorithmic bytes or flops and bound."""
+    the step, at the workload's shape, each with its algorithmic bytes or flops and bound; with
+    ``cpu``, beside each the oracle's time on a bounded sample of the same call, scaled to the
+    whole call."""
     import numpy as np
     import torch
+    from threadpoolctl import threadpool_info
 
     import synth
     from paper_2608_05448_amd import dblast as D
@@ -182,6 +185,15 @@ def _rows(wl, dev, steps: int, warmup: int):
         return {"ms": ms, "bound": "hbm", "bytes": nbytes, "achieved": gbs,
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS}
 
+    def oracle(fn, scale, sample):
+        t0 = time.perf_counter()
+        fn()
+        el = time.perf_counter() - t0
+        threads = max([q.get("num_threads", 1) for q in threadpool_info()] + [1])
+        return {"value": el * scale * 1e3, "unit": "ms per call (sample time x scale)",
+                "cores": min(threads, len(os.sched_getaffinity(0))), "kind": "oracle",
+                "sample": f"{sample}: {el * 1e3:.3f} ms on the host, x{scale:g}"}
+
     rows = {}
     # Branch expander: [B*K, d] x [R*d, d]^T plus bias and residual, bf16 out.
     ht = synth.make_uniform_logits((B, K, d), 11, device=dev).to(torch.bfloat16)
@@ -192,6 +204,12 @@ def _rows(wl, dev, steps: int, warmup: int):
     r = hbm(ms, 2.0 * (R * d * d + B * K * d + R * d + B * K * R * d))
     r["tflops"] = 2.0 * B * K * R * d * d / (ms * 1e-3) / 1e12
     rows["expand_branches"] = r
+    if cpu:
+        from oracle import expander as EX
+        h8 = ht.reshape(B * K, d)[:8].double().cpu().numpy()
+        W64, c64 = We.double().cpu().numpy(), ce.double().cpu().numpy()
+        r["cpu_baseline"] = oracle(lambda: EX.expand_branches(h8, W64, c64, round_bf16=True),
+                                   B * K / 8, f"8 of {B * K} trunk rows")
     # Prior head: category logits from the anchor states.
     U = (synth.make_uniform_logits((R, d), 14, device=dev) * (1.0 / d ** 0.5)).to(torch.bfloat16)
     e = (synth.make_uniform_logits((R,), 15, device=dev) * 0.1).to(torch.bfloat16)
@@ -199,6 +217,11 @@ def _rows(wl, dev, steps: int, warmup: int):
     ha = ht[:, 0].contiguous()
     ms = timed(lambda: D.dbl_prior_head(ha, U, e, out=pl))
     rows["prior_head"] = {"ms": ms, "bound": "latency"}
+    if cpu:
+        from oracle import expander as EX
+        ha64, U64, e64 = ha.double().cpu().numpy(), U.double().cpu().numpy(), e.double().cpu().numpy()
+        rows["prior_head"]["cpu_baseline"] = oracle(lambda: EX.prior_logits(ha64, U64, e64), 1,
+                                                    f"all {B} blocks")
     # Objective forward along target trajectories (head outputs of the step's inputs).
     h = synth.make_h(wl, dev)
     w = synth.make_w(wl, dev)
@@ -209,7 +232,20 @@ def _rows(wl, dev, steps: int, warmup: int):
     xs = synth.make_trajectory(wl, logp)
     ms = timed(lambda: D.dbl_acceptance_objective(tls, lmass, lse, ell, xs, logp, z_temp=wl.z_temp))
     rows["acceptance_objective"] = {"ms": ms, "bound": "latency", "blocks": B}
-    del tls, lmass, lse, h
+    del tls, lmass, lse
+    if cpu:   # the oracle's own head output for one block (not timed), then its objective
+        from oracle import head as OH
+        from oracle import objective as OB
+        w_np = synth.make_w(wl, dev).float().cpu().numpy()
+        t_, l_, s_ = OH.head_factored(h[0].float().cpu().numpy().reshape(K * R, d), w_np,
+                                      v_chunk=8192)
+        del w_np
+        lq1 = OH.flat_logq(t_, l_, s_).reshape(1, K, R, V)
+        e1, x1, lp1 = ell[:1].cpu().numpy(), xs[:1].cpu().numpy(), logp[:1].cpu().numpy()
+        rows["acceptance_objective"]["cpu_baseline"] = oracle(
+            lambda: OB.acceptance_objective(lq1, e1, wl.z_temp, x1, lp1, tau=0.1), B,
+            f"1 of {B} blocks (given the oracle head's log-probs)")
+    del h
     # Target transform on the verification rows (K + 1 per block) with the paper's filters.
     g = synth.make_target_logits(wl, K + 1, device=dev).to(torch.float32)
     lp = torch.empty_like(g)
@@ -217,11 +253,22 @@ def _rows(wl, dev, steps: int, warmup: int):
     for T, k, p in ((0.7, 20, 0.8), (1.0, 20, 0.95), (1.0, 0, 0.95)):
         ms = timed(lambda: D.dbl_target_logprobs(g, T, k, p, out=lp))
         rows[f"target_logprobs_T{T}_k{k}_p{p}"] = hbm(ms, nbytes)
+        if cpu:
+            from oracle import target as TG
+            g4 = g.reshape(-1, V)[:4].cpu().numpy()
+            rows[f"target_logprobs_T{T}_k{k}_p{p}"]["cpu_baseline"] = oracle(
+                lambda: TG.filter_logprobs(g4, T, k, p), B * (K + 1) / 4,
+                f"4 of {B * (K + 1)} rows")
     # Early determinism on the filtered rows.
     rng = np.random.default_rng(0)
     xd = torch.from_numpy(rng.integers(0, V, size=(B, K + 1), dtype=np.int32)).to(dev)
     ms = timed(lambda: D.dbl_early_determinism(xd, lp))
     rows["early_determinism"] = {"ms": ms, "bound": "latency", "blocks": B}
+    if cpu:
+        from oracle import target as TG
+        lpx = np.log(np.random.default_rng(1).uniform(1e-3, 1.0, size=(B, K + 1)))
+        rows["early_determinism"]["cpu_baseline"] = oracle(
+            lambda: TG.early_determinism(lpx), 1, f"all {B} blocks (synthetic gathered log-probs)")
     # Reference rates for the streaming kernels, over as many bytes as the verify stream reads:
     # the library's plain streaming-read probe and a plain device copy.
     del g, lp
@@ -371,7 +418,8 @@ def main(argv=None):
     torch.cuda.set_device(dev)
     D.load()
     if args.mode == "rows":
-        print(json.dumps(_rows(wl, dev, args.steps, args.warmup)), flush=True)
+        print(json.dumps(_rows(wl, dev, args.steps, args.warmup, not args.no_cpu_baseline)),
+              flush=True)
         return 0
     if wl.name == "objective":
         print(json.dumps(_objective_chunks(wl, dev, args.steps, args.warmup)), flush=True)
