@@ -250,9 +250,13 @@ def _rows(wl, dev, steps: int, warmup: int, cpu: bool = True):
     g = synth.make_target_logits(wl, K + 1, device=dev).to(torch.float32)
     lp = torch.empty_like(g)
     nbytes = 2.0 * g.numel() * 4
+    ws_t = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_TARGET, B * (K + 1), 1, 1, 0, V),
+                       dtype=torch.uint8, device=dev)
     for T, k, p in ((0.7, 20, 0.8), (1.0, 20, 0.95), (1.0, 0, 0.95)):
-        ms = timed(lambda: D.dbl_target_logprobs(g, T, k, p, out=lp))
+        ms = timed(lambda: D.dbl_target_logprobs(g, T, k, p, out=lp, ws=ws_t))
         rows[f"target_logprobs_T{T}_k{k}_p{p}"] = hbm(ms, nbytes)
+        ms1 = timed(lambda: D.dbl_target_logprobs(g, T, k, p, out=lp, split=False))
+        rows[f"target_logprobs_T{T}_k{k}_p{p}"]["ms_one_workgroup_per_row"] = ms1
         if cpu:
             from oracle import target as TG
             g4 = g.reshape(-1, V)[:4].cpu().numpy()

@@ -99,7 +99,8 @@ typedef enum {
   DBL_OP_EXPECTED_LEN = 3,
   DBL_OP_SAMPLE_GREEDY = 4,
   DBL_OP_VERIFY_GREEDY = 5,
-  DBL_OP_EXPECTED_LEN_GREEDY = 6
+  DBL_OP_EXPECTED_LEN_GREEDY = 6,
+  DBL_OP_TARGET = 7              /* dbl_target_logprobs: rows N = shape.B * shape.K, shape.V */
 } dbl_op;
 
 typedef struct {
@@ -331,12 +332,19 @@ dbl_status dbl_prior_head(dbl_shape shape, const void* h_anchor, const void* U, 
  * kept of exp(s - max)) in binary64, -inf outside the kept set. T = 0 keeps only the lowest-index
  * maximum (log p = 0 there). The kept set is exact and independent of evaluation order.
  *   N, V         rows and vocabulary size (1 <= V < 2^24)
- *   logits       [N, V] fp32 target logits;  logp  out [N, V] fp32 (may alias logits)
+ *   logits       [N, V] fp32 target logits;  logp  out [N, V] fp32, must not overlap logits
+ *                (the row is written before the last reads of it)
  *   temperature  finite, >= 0;  top_k  >= 0 (0: off);  top_p  in (0, 1] (1: off)
- * No workspace. Errors: DBL_EINVAL for null pointers or parameters out of range; DBL_ESHAPE.
+ *   ws, ws_bytes optional workspace: NULL and 0, or dbl_workspace_bytes(DBL_OP_TARGET, shape)
+ *                bytes (256-byte aligned) with shape.B * shape.K = N, shape.V = V. With it, rows
+ *                with 0 < top_k <= 256 and V >= 16384 are split over several workgroups
+ *                (faster when N is near or below the number of CUs); the output is the same.
+ * Errors: DBL_EINVAL for null pointers, overlapping logits and logp, or parameters out of range;
+ * DBL_ESHAPE; DBL_EWORKSPACE for a workspace that is too small or misaligned.
  */
 dbl_status dbl_target_logprobs(int64_t N, int64_t V, const float* logits, float temperature,
-                               int64_t top_k, float top_p, float* logp, void* stream);
+                               int64_t top_k, float top_p, float* logp, void* ws,
+                               size_t ws_bytes, void* stream);
 
 /*
  * dbl_early_determinism - target-block early determinism (appendix "Target-Block Early

@@ -87,6 +87,11 @@ WsLayout layout(int op, const dbl_shape& s) {
       sizes[1] = B * K * nchunk * sizeof(float);
       n = 2;
       break;
+    case DBL_OP_TARGET:  // rows B*K: per-segment candidate lists and their counts
+      sizes[0] = B * K * dbl::kFilterSegs * dbl::kFilterSegCap * sizeof(uint64_t);
+      sizes[1] = B * K * dbl::kFilterSegs * sizeof(int32_t);
+      n = 2;
+      break;
     default:
       L.total = SIZE_MAX;
       return L;
@@ -425,15 +430,28 @@ dbl_status dbl_prior_head(dbl_shape s, const void* h_anchor, const void* U, cons
 }
 
 dbl_status dbl_target_logprobs(int64_t N, int64_t V, const float* logits, float temperature,
-                               int64_t top_k, float top_p, float* logp, void* stream) {
+                               int64_t top_k, float top_p, float* logp, void* ws,
+                               size_t ws_bytes, void* stream) {
   if (N < 0 || V < 1 || V >= (int64_t(1) << 24)) return fail(DBL_ESHAPE, "need N >= 0, 1 <= V < 2^24");
   if (static_cast<double>(N) * static_cast<double>(V) >= 4.0e18)
     return fail(DBL_ESHAPE, "N*V too large");
   if (!logits || !logp) return fail(DBL_EINVAL, "NULL pointer");
+  {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(logits), b0 = reinterpret_cast<uintptr_t>(logp);
+    const uintptr_t len = static_cast<uintptr_t>(N) * static_cast<uintptr_t>(V) * sizeof(float);
+    if (len > 0 && a0 < b0 + len && b0 < a0 + len)
+      return fail(DBL_EINVAL, "logp must not overlap logits");
+  }
   if (!(temperature >= 0.0f) || isinf(temperature))
     return fail(DBL_EINVAL, "temperature must be finite and >= 0");
   if (top_k < 0) return fail(DBL_EINVAL, "top_k must be >= 0");
   if (!(top_p > 0.0f && top_p <= 1.0f)) return fail(DBL_EINVAL, "top_p must be in (0, 1]");
+  WsLayout L;
+  const bool use_ws = ws != nullptr || ws_bytes != 0;
+  if (use_ws) {
+    const dbl_shape rows{N, 1, 1, 0, V};
+    if (dbl_status st = check_ws(DBL_OP_TARGET, rows, ws, ws_bytes, &L)) return st;
+  }
   if (N == 0) return ok();
   dbl::FilterArgs a;
   a.N = N;
@@ -443,6 +461,10 @@ dbl_status dbl_target_logprobs(int64_t N, int64_t V, const float* logits, float 
   a.top_k = top_k;
   a.top_p = top_p;
   a.logp = logp;
+  if (use_ws) {
+    a.seg_cand = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + L.off[0]);
+    a.seg_count = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + L.off[1]);
+  }
   return hip_status(dbl::launch_filter(a, static_cast<hipStream_t>(stream)), "filter launch");
 }
 

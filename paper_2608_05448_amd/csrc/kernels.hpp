@@ -115,6 +115,11 @@ struct PriorHeadArgs {
 };
 
 // Target sampling transform: rows of logits -> filtered log-probabilities.
+// Rows of the target transform split over kFilterSegs workgroups keep up to kFilterSegCap
+// candidates each in the workspace.
+constexpr int kFilterSegs = 4;
+constexpr int kFilterSegCap = 1024;
+
 struct FilterArgs {
   int64_t N, V;
   const float* logits;  // [N, V]
@@ -122,6 +127,8 @@ struct FilterArgs {
   int64_t top_k;        // 0: off
   float top_p;          // 1: off
   float* logp;          // [N, V]
+  uint64_t* seg_cand = nullptr;   // workspace [N, kFilterSegs, kFilterSegCap] or null
+  int32_t* seg_count = nullptr;   // workspace [N, kFilterSegs]
 };
 
 // Early-determinism estimate from sampled target blocks.

@@ -184,6 +184,192 @@ __device__ __forceinline__ uint32_t wave_kth_largest(uint32_t t0, uint32_t t1, u
 constexpr int kFastK = 1024;
 constexpr int kCandCap = 4096;
 
+// Sorts a candidate list - visiting keys (key of s, ~id) of every token whose s is at least a
+// lower bound of the row's k-th largest s - in visiting order (s descending, id ascending),
+// applies both cuts and writes the kept tokens' log-probabilities; the rest of the output row
+// already holds -inf. Needs n >= k and n <= kCandCap; all kFT threads call it.
+// Wavefront 0 alone, when the tokens tied with or above the k-th largest s number at most 64
+// (the usual case for small k): those nk tokens are gathered one per lane, sorted in visiting
+// order with a register bitonic network, and both cuts and the normaliser are wavefront
+// reductions, with no workgroup barrier. tk is the k-th largest key of the list.
+__device__ void finish_small(const FilterArgs& a, float* out, uint64_t* cand, int n,
+                             uint32_t tk, int nk) {
+  const int lane = lane_id();
+  // compact the nk entries with key >= tk to the front of the list, in list order (an entry
+  // moves only towards the front, past entries this wavefront has already read)
+  int base = 0;
+  for (int i0 = 0; i0 < n; i0 += 64) {
+    const int i = i0 + lane;
+    const uint64_t c = i < n ? cand[i] : 0;
+    const bool in = i < n && static_cast<uint32_t>(c >> 32) >= tk;
+    const uint64_t msk = __ballot(in);
+    if (in) cand[base + __popcll(msk & ((1ull << lane) - 1))] = c;
+    base += __popcll(msk);
+    asm volatile("" ::: "memory");
+  }
+  uint64_t e = lane < nk ? cand[lane] : 0;
+  // bitonic sort, descending, of one entry per lane (empty lanes hold 0)
+#pragma unroll
+  for (int size = 2; size <= 64; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const uint64_t o = __shfl_xor(e, stride);
+      const bool desc = (lane & size) == 0;
+      const bool lower = (lane & stride) == 0;
+      e = (lower == desc) ? (e > o ? e : o) : (e < o ? e : o);
+    }
+  }
+  const float sv = key_value(static_cast<uint32_t>(e >> 32));
+  const float m = __shfl(sv, 0);
+  int nkeep = nk;
+  if (a.top_p < 1.0f) {
+    const uint64_t P = lane < nk ? quant40(detexp32(__fsub_rn(sv, m))) : 0;
+    const uint64_t incl = wave_incl_scan_u64(P);
+    const uint64_t z = __shfl(incl, 63);
+    uint64_t tp = static_cast<uint64_t>(ceil(__dmul_rn(static_cast<double>(a.top_p),
+                                                       static_cast<double>(z))));
+    if (tp == 0) tp = 1;
+    nkeep = __popcll(__ballot(lane < nk && incl - P < tp));
+  }
+  const double x = lane < nkeep ? exp(static_cast<double>(sv) - static_cast<double>(m)) : 0.0;
+  const double lse = log(wave_sum_f64(x));
+  if (lane < nkeep) {
+    const int64_t v = 0xFFFFFFFFu - static_cast<uint32_t>(e);
+    out[v] = static_cast<float>(static_cast<double>(sv) - static_cast<double>(m) - lse);
+  }
+}
+
+__device__ void finish_candidates(const FilterArgs& a, float* out, uint64_t* cand, int n,
+                                  uint64_t* red, double* redd, int* sh_n) {
+  const int tid = threadIdx.x;
+  const int k = static_cast<int>(a.top_k);
+  // Wavefront 0: the k-th largest key of the list (bisection with ballots over the list) and
+  // how many entries are at or above it.
+  if (tid < 64) {
+    uint64_t lo = 0, hi = 0xFFFFFFFFu;
+    int c = 0;
+    if (n <= 8 * 64) {  // up to 8 keys per lane, in registers; counts by ballot
+      uint32_t kk[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int i = tid + 64 * j;
+        kk[j] = i < n ? static_cast<uint32_t>(cand[i] >> 32) : 0;
+      }
+      auto count = [&](uint32_t t) {
+        int r = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) r += __popcll(__ballot(kk[j] >= t && tid + 64 * j < n));
+        return r;
+      };
+      while (lo < hi) {
+        const uint64_t mid = lo + (hi - lo + 1) / 2;
+        if (count(static_cast<uint32_t>(mid)) >= k) lo = mid; else hi = mid - 1;
+      }
+      c = count(static_cast<uint32_t>(lo));
+    } else {
+      auto count = [&](uint64_t t) {
+        int r = 0;
+        for (int i = tid; i < n; i += 64) r += static_cast<uint32_t>(cand[i] >> 32) >= t ? 1 : 0;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) r += __shfl_xor(r, o);
+        return r;
+      };
+      while (lo < hi) {
+        const uint64_t mid = lo + (hi - lo + 1) / 2;
+        if (count(mid) >= k) lo = mid; else hi = mid - 1;
+      }
+      c = count(lo);
+    }
+    if (tid == 0) {
+      red[0] = lo;
+      red[1] = static_cast<uint64_t>(c);
+    }
+  }
+  __syncthreads();
+  const uint32_t tk0 = static_cast<uint32_t>(red[0]);
+  const int nk0 = static_cast<int>(red[1]);
+  __syncthreads();
+  if (nk0 <= 64) {
+    if (tid < 64) finish_small(a, out, cand, n, tk0, nk0);
+    return;
+  }
+  // bitonic sort, descending, of the list padded with zeros to a power of two (every real
+  //    entry has a nonzero low word, ids being below 2^32 - 1)
+  int np = 64;
+  while (np < n) np <<= 1;
+  for (int i = n + tid; i < np; i += kFT) cand[i] = 0;
+  __syncthreads();
+  for (int size = 2; size <= np; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < (np >> 1); i += kFT) {
+        const int i0 = 2 * i - (i & (stride - 1));  // the pair (i0, i0 + stride)
+        const int i1 = i0 + stride;
+        const bool desc = (i0 & size) == 0;
+        const uint64_t x = cand[i0], y = cand[i1];
+        if ((x < y) == desc) {
+          cand[i0] = y;
+          cand[i1] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  auto key_at = [&](int i) { return static_cast<uint32_t>(cand[i] >> 32); };
+  const float m = key_value(key_at(0));
+  // top-k: the first k entries and every later one tied with the k-th (n >= k: the list holds
+  // every token at or above the row's k-th largest key)
+  const uint32_t tk = key_at(k - 1);
+  int nk = k;
+  while (nk < n && key_at(nk) >= tk) ++nk;
+  int nkeep = nk;
+  if (a.top_p < 1.0f) {
+    // integer masses of the first nk entries, four per thread in list order; a token is kept
+    // while the mass before it is below T_p = ceil(p Z)
+    uint64_t P[4], loc = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = 4 * tid + j;
+      P[j] = i < nk ? quant40(detexp32(__fsub_rn(key_value(key_at(i)), m))) : 0;
+      loc += P[j];
+    }
+    const uint64_t incl = wave_incl_scan_u64(loc);
+    if (lane_id() == 63) red[tid >> 6] = incl;
+    __syncthreads();
+    uint64_t base = 0, z = 0;
+#pragma unroll
+    for (int w = 0; w < kFW; ++w) {
+      const uint64_t r = red[w];
+      base += w < (tid >> 6) ? r : 0;
+      z += r;
+    }
+    __syncthreads();
+    uint64_t tp = static_cast<uint64_t>(ceil(__dmul_rn(static_cast<double>(a.top_p),
+                                                       static_cast<double>(z))));
+    if (tp == 0) tp = 1;
+    uint64_t before = base + incl - loc;
+    uint64_t c = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (4 * tid + j < nk) {
+        c += before < tp ? 1 : 0;
+        before += P[j];
+      }
+    }
+    nkeep = static_cast<int>(block_sum_u64(c, red));
+  }
+  double se = 0.0;
+  for (int i = tid; i < nkeep; i += kFT)
+    se += exp(static_cast<double>(key_value(key_at(i))) - static_cast<double>(m));
+  const double lse = log(block_sum_f64(se, redd));
+  // kept tokens (the first nkeep entries of the list)
+  for (int i = tid; i < nkeep; i += kFT) {
+    const uint64_t e = cand[i];
+    const int64_t v = 0xFFFFFFFFu - static_cast<uint32_t>(e);
+    out[v] = static_cast<float>(static_cast<double>(key_value(static_cast<uint32_t>(e >> 32))) -
+                                static_cast<double>(m) - lse);
+  }
+}
+
 __device__ bool filter_fast(const FilterArgs& a, const float* in, float* out, bool vec,
                             uint64_t* cand, int* resc, uint64_t* red, double* redd, int* sh_n,
                             int* sh_r) {
@@ -318,119 +504,19 @@ __device__ bool filter_fast(const FilterArgs& a, const float* in, float* out, bo
   const int n = *sh_n;
   __syncthreads();
   if (n > kCandCap) return false;
-  // 4. bitonic sort, descending, of the list padded with zeros to a power of two (every real
-  //    entry has a nonzero low word, ids being below 2^32 - 1)
-  int np = 64;
-  while (np < n) np <<= 1;
-  for (int i = n + tid; i < np; i += kFT) cand[i] = 0;
-  __syncthreads();
-  for (int size = 2; size <= np; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < (np >> 1); i += kFT) {
-        const int i0 = 2 * i - (i & (stride - 1));  // the pair (i0, i0 + stride)
-        const int i1 = i0 + stride;
-        const bool desc = (i0 & size) == 0;
-        const uint64_t x = cand[i0], y = cand[i1];
-        if ((x < y) == desc) {
-          cand[i0] = y;
-          cand[i1] = x;
-        }
-      }
-      __syncthreads();
-    }
-  }
-  auto key_at = [&](int i) { return static_cast<uint32_t>(cand[i] >> 32); };
-  const float m = key_value(key_at(0));
-  // top-k: the first k entries and every later one tied with the k-th (n >= k: the list holds
-  // every token at or above the row's k-th largest key)
-  const uint32_t tk = key_at(k - 1);
-  int nk = k;
-  while (nk < n && key_at(nk) >= tk) ++nk;
-  int nkeep = nk;
-  if (a.top_p < 1.0f) {
-    // integer masses of the first nk entries, four per thread in list order; a token is kept
-    // while the mass before it is below T_p = ceil(p Z)
-    uint64_t P[4], loc = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = 4 * tid + j;
-      P[j] = i < nk ? quant40(detexp32(__fsub_rn(key_value(key_at(i)), m))) : 0;
-      loc += P[j];
-    }
-    const uint64_t incl = wave_incl_scan_u64(loc);
-    if (lane_id() == 63) red[tid >> 6] = incl;
-    __syncthreads();
-    uint64_t base = 0, z = 0;
-#pragma unroll
-    for (int w = 0; w < kFW; ++w) {
-      const uint64_t r = red[w];
-      base += w < (tid >> 6) ? r : 0;
-      z += r;
-    }
-    __syncthreads();
-    uint64_t tp = static_cast<uint64_t>(ceil(__dmul_rn(static_cast<double>(a.top_p),
-                                                       static_cast<double>(z))));
-    if (tp == 0) tp = 1;
-    uint64_t before = base + incl - loc;
-    uint64_t c = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (4 * tid + j < nk) {
-        c += before < tp ? 1 : 0;
-        before += P[j];
-      }
-    }
-    nkeep = static_cast<int>(block_sum_u64(c, red));
-  }
-  double se = 0.0;
-  for (int i = tid; i < nkeep; i += kFT)
-    se += exp(static_cast<double>(key_value(key_at(i))) - static_cast<double>(m));
-  const double lse = log(block_sum_f64(se, redd));
-  // 5. kept tokens (the first nkeep entries of the list)
-  for (int i = tid; i < nkeep; i += kFT) {
-    const uint64_t e = cand[i];
-    const int64_t v = 0xFFFFFFFFu - static_cast<uint32_t>(e);
-    out[v] = static_cast<float>(static_cast<double>(key_value(static_cast<uint32_t>(e >> 32))) -
-                                static_cast<double>(m) - lse);
-  }
+  finish_candidates(a, out, cand, n, red, redd, sh_n);
   return true;
 }
 
-__global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
-  __shared__ uint64_t hist[256];
-  __shared__ uint64_t cand[kCandCap];
-  __shared__ int resc[kFT];
-  __shared__ int sh_n, sh_r;
-  __shared__ uint64_t red[kFW];
-  __shared__ double redd[kFW];
-  __shared__ uint32_t sh_digit;
-  __shared__ uint64_t sh_above;
-  const int64_t n = blockIdx.x;
-  const int64_t V = a.V;
-  const float* in = a.logits + n * V;
-  float* out = a.logp + n * V;
+// General path: exact radix selections over the keys of s (every k, and the nucleus alone),
+// reading the row several times and writing all of it.
+__device__ void filter_general(const FilterArgs& a, const float* in, float* out, bool vec,
+                               uint64_t* hist, uint64_t* red, double* redd, uint32_t* sh_digit,
+                               uint64_t* sh_above) {
   const int tid = threadIdx.x;
-
-  if (a.temperature == 0.0f) {  // lowest-index maximum
-    uint64_t best = 0;
-    for (int64_t v = tid; v < V; v += kFT) {
-      const uint64_t k = (static_cast<uint64_t>(order_key(in[v])) << 32) |
-                         (0xFFFFFFFFu - static_cast<uint32_t>(v));
-      best = k > best ? k : best;
-    }
-    best = block_max_u64(best, red);
-    const int64_t arg = 0xFFFFFFFFu - static_cast<uint32_t>(best);
-    for (int64_t v = tid; v < V; v += kFT) out[v] = v == arg ? 0.0f : -INFINITY;
-    return;
-  }
+  const int64_t V = a.V;
   const float T = a.temperature;
   auto s_of = [&](int64_t v) { return __fdiv_rn(in[v], T); };
-  const bool vec = (V & 3) == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
-                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
-  if (a.top_k > 0 && a.top_k <= kFastK && a.top_k < V &&
-      filter_fast(a, in, out, vec, cand, resc, red, redd, &sh_n, &sh_r))
-    return;
-
   // Row maximum (key of the largest s).
   uint32_t mk = 0;
   row_scan<4>(in, V, T, vec, [&](int64_t, float sv) {
@@ -456,7 +542,7 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
       __syncthreads();
       uint32_t d;
       uint64_t above;
-      pick_digit(hist, need, &d, &above, &sh_digit, &sh_above);
+      pick_digit(hist, need, &d, &above, sh_digit, sh_above);
       need -= above;
       prefix |= d << shift;
       pmask |= 255u << shift;
@@ -494,7 +580,7 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
       }
       uint32_t d;
       uint64_t above;
-      pick_digit(hist, need, &d, &above, &sh_digit, &sh_above);
+      pick_digit(hist, need, &d, &above, sh_digit, sh_above);
       need -= above;
       if (shift == 0) tie_mass = hist[d];
       prefix |= d << shift;
@@ -562,6 +648,199 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
   });
 }
 
+__global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
+  __shared__ uint64_t hist[256];
+  __shared__ uint64_t cand[kCandCap];
+  __shared__ int resc[kFT];
+  __shared__ int sh_n, sh_r;
+  __shared__ uint64_t red[kFW];
+  __shared__ double redd[kFW];
+  __shared__ uint32_t sh_digit;
+  __shared__ uint64_t sh_above;
+  const int64_t n = blockIdx.x;
+  const int64_t V = a.V;
+  const float* in = a.logits + n * V;
+  float* out = a.logp + n * V;
+  const int tid = threadIdx.x;
+
+  if (a.temperature == 0.0f) {  // lowest-index maximum
+    uint64_t best = 0;
+    for (int64_t v = tid; v < V; v += kFT) {
+      const uint64_t k = (static_cast<uint64_t>(order_key(in[v])) << 32) |
+                         (0xFFFFFFFFu - static_cast<uint32_t>(v));
+      best = k > best ? k : best;
+    }
+    best = block_max_u64(best, red);
+    const int64_t arg = 0xFFFFFFFFu - static_cast<uint32_t>(best);
+    for (int64_t v = tid; v < V; v += kFT) out[v] = v == arg ? 0.0f : -INFINITY;
+    return;
+  }
+  const bool vec = (V & 3) == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  if (a.top_k > 0 && a.top_k <= kFastK && a.top_k < V &&
+      filter_fast(a, in, out, vec, cand, resc, red, redd, &sh_n, &sh_r))
+    return;
+
+  filter_general(a, in, out, vec, hist, red, redd, &sh_digit, &sh_above);
+}
+
+// Rows split over kFilterSegs workgroups (0 < k <= 256, with a workspace). A segment
+// workgroup streams its share of the row once (writing -inf, keeping each thread's four
+// largest logit keys), bounds its share's k-th largest key from below (the largest over its
+// wavefronts of each wavefront's k-th largest held key), and appends every token of its share
+// at or above that bound (in s) to the row's candidate lists in the workspace: the row's top-k
+// tokens of that share are among them, the share's k-th largest being at most the row's. A
+// merge workgroup per row then sorts the lists and writes the kept tokens. A list that
+// overflows sends the row to the general path.
+constexpr int kSegThreads = 512;
+constexpr int kSegWaves = kSegThreads / 64;
+
+__global__ __launch_bounds__(kSegThreads) void filter_seg_kernel(FilterArgs a) {
+  __shared__ int resc[kSegThreads];
+  __shared__ int sh_n, sh_r;
+  __shared__ uint32_t redk[kSegWaves];
+  const int64_t row = blockIdx.x / kFilterSegs;
+  const int seg = static_cast<int>(blockIdx.x % kFilterSegs);
+  const int tid = threadIdx.x;
+  const int64_t V = a.V;
+  const float T = a.temperature;
+  const int k = static_cast<int>(a.top_k);
+  const float* in = a.logits + row * V;
+  float* out = a.logp + row * V;
+  const bool vec = (V & 3) == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  // This workgroup's units (float4 groups, or single ids): [u0, u1), thread t owns
+  // u0 + t + i * kSegThreads.
+  const int64_t units = vec ? (V >> 2) : V;
+  const int64_t per = (units + kFilterSegs - 1) / kFilterSegs;
+  const int64_t u0 = min(units, seg * per), u1 = min(units, u0 + per);
+  uint32_t t0 = 0, t1 = 0, t2 = 0, t3 = 0;
+  auto insert = [&](float lv) {
+    uint32_t x = order_key(lv);
+    uint32_t y = max(t0, x);
+    x = min(t0, x);
+    t0 = y;
+    y = max(t1, x);
+    x = min(t1, x);
+    t1 = y;
+    y = max(t2, x);
+    x = min(t2, x);
+    t2 = y;
+    t3 = max(t3, x);
+  };
+  if (vec) {
+    const float4* in4 = reinterpret_cast<const float4*>(in);
+    float4* out4 = reinterpret_cast<float4*>(out);
+    const float4 ninf = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    int64_t j = u0 + tid;
+    for (; j + (kBatch - 1) * kSegThreads < u1; j += kBatch * kSegThreads) {
+      float4 x[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) x[u] = in4[j + u * kSegThreads];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        out4[j + u * kSegThreads] = ninf;
+        insert(x[u].x);
+        insert(x[u].y);
+        insert(x[u].z);
+        insert(x[u].w);
+      }
+    }
+    for (; j < u1; j += kSegThreads) {
+      const float4 x = in4[j];
+      out4[j] = ninf;
+      insert(x.x);
+      insert(x.y);
+      insert(x.z);
+      insert(x.w);
+    }
+  } else {
+    for (int64_t v = u0 + tid; v < u1; v += kSegThreads) {
+      insert(in[v]);
+      out[v] = -INFINITY;
+    }
+  }
+  // Lower bound of this share's k-th largest logit key.
+  const uint32_t kw = wave_kth_largest(t0, t1, t2, t3, k);
+  if (lane_id() == 0) redk[tid >> 6] = kw;
+  if (tid == 0) {
+    sh_n = 0;
+    sh_r = 0;
+  }
+  __syncthreads();
+  uint32_t tlow = 0;
+#pragma unroll
+  for (int w = 0; w < kSegWaves; ++w) tlow = max(tlow, redk[w]);
+  const uint32_t x_low = least_logit_key(order_key(__fdiv_rn(key_value(tlow), T)), T);
+  if (t0 >= x_low) resc[atomicAdd(&sh_r, 1)] = tid;
+  __syncthreads();
+  // Re-read the listed threads' units, spread over the workgroup.
+  const int nr = sh_r;
+  const int G = static_cast<int>((u1 - u0 + kSegThreads - 1) / kSegThreads);
+  const int64_t items = static_cast<int64_t>(nr) * G;
+  uint64_t* list = a.seg_cand + blockIdx.x * static_cast<int64_t>(kFilterSegCap);
+  auto take = [&](int64_t v, float lv) {
+    if (order_key(lv) >= x_low) {
+      const int slot = atomicAdd(&sh_n, 1);
+      if (slot < kFilterSegCap) list[slot] = visit_key(order_key(__fdiv_rn(lv, T)), v);
+    }
+  };
+  for (int64_t w = tid; w < items; w += kSegThreads) {
+    const int64_t j = u0 + resc[w / G] + (w % G) * static_cast<int64_t>(kSegThreads);
+    if (j >= u1) continue;
+    if (vec) {
+      const float4 x = reinterpret_cast<const float4*>(in)[j];
+      take(4 * j, x.x);
+      take(4 * j + 1, x.y);
+      take(4 * j + 2, x.z);
+      take(4 * j + 3, x.w);
+    } else {
+      take(j, in[j]);
+    }
+  }
+  __syncthreads();
+  if (tid == 0) a.seg_count[blockIdx.x] = sh_n;
+}
+
+// One workgroup per row: the row's segment lists, merged and finished; or the general path
+// when a list overflowed.
+__global__ __launch_bounds__(kFT) void filter_merge_kernel(FilterArgs a) {
+  __shared__ uint64_t hist[256];
+  __shared__ uint64_t cand[kCandCap];
+  __shared__ int sh_n;
+  __shared__ uint64_t red[kFW];
+  __shared__ double redd[kFW];
+  __shared__ uint32_t sh_digit;
+  __shared__ uint64_t sh_above;
+  const int64_t row = blockIdx.x;
+  const int64_t V = a.V;
+  const float* in = a.logits + row * V;
+  float* out = a.logp + row * V;
+  int cnt[kFilterSegs], n = 0;
+  bool over = false;
+#pragma unroll
+  for (int sgi = 0; sgi < kFilterSegs; ++sgi) {
+    cnt[sgi] = a.seg_count[row * kFilterSegs + sgi];
+    over = over || cnt[sgi] > kFilterSegCap;
+    n += cnt[sgi];
+  }
+  if (over) {
+    const bool vec = (V & 3) == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+                     (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+    filter_general(a, in, out, vec, hist, red, redd, &sh_digit, &sh_above);
+    return;
+  }
+  int base = 0;
+#pragma unroll
+  for (int sgi = 0; sgi < kFilterSegs; ++sgi) {
+    const uint64_t* list = a.seg_cand + (row * kFilterSegs + sgi) * static_cast<int64_t>(kFilterSegCap);
+    for (int i = threadIdx.x; i < cnt[sgi]; i += kFT) cand[base + i] = list[i];
+    base += cnt[sgi];
+  }
+  __syncthreads();
+  finish_candidates(a, out, cand, n, red, redd, &sh_n);
+}
+
 // Per sampled block: (1/b) sum_j prod_{i<=j} p(x_i); one thread per block.
 __global__ __launch_bounds__(256) void determinism_terms_kernel(DeterminismArgs a) {
   const int64_t mblk = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -590,8 +869,19 @@ __global__ __launch_bounds__(kFT) void determinism_mean_kernel(DeterminismArgs a
 }  // namespace
 
 hipError_t launch_filter(const FilterArgs& a, hipStream_t stream) {
-  if (a.N > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(filter_kernel, dim3(static_cast<unsigned>(a.N)), dim3(kFT), 0, stream, a);
+  if (a.N > 0x7fffffff / kFilterSegs) return hipErrorInvalidConfiguration;
+  const bool split = a.seg_cand && a.seg_count && a.temperature > 0.0f && a.top_k > 0 &&
+                     a.top_k <= 256 && a.top_k < a.V && a.V >= kFilterSegs * 4096;
+  if (!split) {
+    hipLaunchKernelGGL(filter_kernel, dim3(static_cast<unsigned>(a.N)), dim3(kFT), 0, stream, a);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(filter_seg_kernel, dim3(static_cast<unsigned>(a.N * kFilterSegs)),
+                     dim3(kSegThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(filter_merge_kernel, dim3(static_cast<unsigned>(a.N)), dim3(kFT), 0, stream,
+                     a);
   return hipGetLastError();
 }
 

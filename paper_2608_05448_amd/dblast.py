@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libdblast.so")
 DBL_OK, DBL_EINVAL, DBL_ESHAPE, DBL_EDTYPE, DBL_EWORKSPACE, DBL_EHIP = range(6)
 DBL_F32, DBL_BF16 = 0, 1
 (DBL_OP_HEAD, DBL_OP_SAMPLE, DBL_OP_VERIFY, DBL_OP_EXPECTED_LEN, DBL_OP_SAMPLE_GREEDY,
- DBL_OP_VERIFY_GREEDY, DBL_OP_EXPECTED_LEN_GREEDY) = range(7)
+ DBL_OP_VERIFY_GREEDY, DBL_OP_EXPECTED_LEN_GREEDY, DBL_OP_TARGET) = range(8)
 VTILE = 128
 
 
@@ -61,7 +61,7 @@ _SIGS = {
                                                 _P, _P, _P, _P]),
     "dbl_expand_branches": (ctypes.c_int, [Shape, _P, _P, _P, _P, _P]),
     "dbl_prior_head": (ctypes.c_int, [Shape, _P, _P, _P, _P, _P]),
-    "dbl_target_logprobs": (ctypes.c_int, [_I64, _I64, _P, _F, _I64, _F, _P, _P]),
+    "dbl_target_logprobs": (ctypes.c_int, [_I64, _I64, _P, _F, _I64, _F, _P, _P, _SZ, _P]),
     "dbl_early_determinism": (ctypes.c_int, [_I64, _I64, _I64, _P, _P, _P, _P, _P]),
     "dbl_stream_read_probe": (ctypes.c_int, [_P, _I64, _P, _I64, _P]),
 }
@@ -375,15 +375,23 @@ def dbl_prior_head(h_anchor, U, e, out=None):
     return out
 
 
-def dbl_target_logprobs(logits, temperature=1.0, top_k=0, top_p=1.0, out=None):
-    """Target sampling log-probabilities for logits [..., V] fp32 (temperature, top-k, top-p)."""
+def dbl_target_logprobs(logits, temperature=1.0, top_k=0, top_p=1.0, out=None, ws=None,
+                        split=True):
+    """Target sampling log-probabilities for logits [..., V] fp32 (temperature, top-k, top-p).
+    ``out`` must not overlap ``logits``. With ``split`` (default) a workspace (``ws`` or a new
+    one) lets rows be split over several workgroups; the result is the same either way."""
     _need(logits, "logits", torch.float32)
     V = logits.shape[-1]
     N = logits.numel() // V
     out = torch.empty_like(logits) if out is None else out
     _need(out, "out", torch.float32, tuple(logits.shape))
+    if split:
+        ws, nws = _workspace(DBL_OP_TARGET, Shape(N, 1, 1, 0, V), logits.device, ws)
+    else:
+        ws, nws = None, 0
     _check(load().dbl_target_logprobs(N, V, _ptr(logits), float(temperature), int(top_k),
-                                      float(top_p), _ptr(out), _stream(logits.device)))
+                                      float(top_p), _ptr(out), _ptr(ws), nws,
+                                      _stream(logits.device)))
     return out
 
 

@@ -58,7 +58,12 @@ def test_workspace_sizes(lib):
     v = lib.dbl_workspace_bytes(D.DBL_OP_VERIFY, S(16, 16, 8, 0, 151936))
     e = lib.dbl_workspace_bytes(D.DBL_OP_EXPECTED_LEN, S(16, 16, 8, 0, 151936))
     assert v > e > 0 and v % 256 == 0 and e % 256 == 0
-    assert lib.dbl_workspace_bytes(7, S(1, 1, 1, 8, 8)) == SIZE_MAX
+    # Target transform: per row, 4 segment lists of 1024 uint64 candidates and 4 int32 counts.
+    assert lib.dbl_workspace_bytes(D.DBL_OP_TARGET, S(272, 1, 1, 0, 151936)) == \
+        272 * 4 * 1024 * 8 + -(-272 * 4 * 4 // 256) * 256
+    assert lib.dbl_workspace_bytes(D.DBL_OP_TARGET, S(16, 17, 1, 0, 151936)) == \
+        lib.dbl_workspace_bytes(D.DBL_OP_TARGET, S(272, 1, 1, 0, 151936))
+    assert lib.dbl_workspace_bytes(8, S(1, 1, 1, 8, 8)) == SIZE_MAX
     assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, S(1, 1, 65, 8, 8)) == SIZE_MAX
     assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, S(0, 4, 2, 8, 256)) == 0
 
@@ -216,3 +221,24 @@ def test_read_probe_validation(lib):
     assert lib.dbl_stream_read_probe(p[0], 64, p[1], (1 << 20) + 1, null) == D.DBL_ESHAPE
     assert lib.dbl_stream_read_probe(ctypes.c_void_p(p[0].value + 4), 64, p[1], 4,
                                      null) == D.DBL_EINVAL
+
+
+def test_target_validation(lib):
+    p = _fake(3)
+    null = ctypes.c_void_p(None)
+    N, V = 4, 1000
+    # logp overlapping logits (same buffer, or shifted inside it)
+    assert lib.dbl_target_logprobs(N, V, p[0], 1.0, 20, 0.9, p[0], null, 0, null) == D.DBL_EINVAL
+    shifted = ctypes.c_void_p(p[0].value + 4 * V)
+    assert lib.dbl_target_logprobs(N, V, p[0], 1.0, 20, 0.9, shifted, null, 0, null) == \
+        D.DBL_EINVAL
+    far = ctypes.c_void_p(p[0].value + 4 * N * V)   # adjacent, not overlapping: only ws fails
+    need = lib.dbl_workspace_bytes(D.DBL_OP_TARGET, D.Shape(N, 1, 1, 0, V))
+    assert lib.dbl_target_logprobs(N, V, p[0], 1.0, 20, 0.9, far, p[2], need - 1, null) == \
+        D.DBL_EWORKSPACE
+    assert lib.dbl_target_logprobs(N, V, p[0], 1.0, 20, 0.9, far, null, need, null) == \
+        D.DBL_EWORKSPACE
+    assert lib.dbl_target_logprobs(N, V, p[0], -1.0, 20, 0.9, far, null, 0, null) == D.DBL_EINVAL
+    assert lib.dbl_target_logprobs(N, V, p[0], 1.0, -1, 0.9, far, null, 0, null) == D.DBL_EINVAL
+    assert lib.dbl_target_logprobs(N, V, p[0], 1.0, 20, 0.0, far, null, 0, null) == D.DBL_EINVAL
+    assert lib.dbl_target_logprobs(0, V, p[0], 1.0, 20, 0.9, far, null, 0, null) == D.DBL_OK

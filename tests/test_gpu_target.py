@@ -53,17 +53,27 @@ CASES = [
     ("one-ulp-neighbours-t07", 4, 30000, 0.7, 20, 0.95, "ulp"),
     ("temperature-3e4-merges-values", 4, 30000, 3e4, 20, 0.95, False),
     ("temperature-1e-3", 4, 30000, 1e-3, 20, 0.9, False),
+    ("split-k256", 3, 151936, 1.0, 256, 0.95, False),
+    ("split-k257", 3, 151936, 1.0, 257, 0.95, False),
+    ("split-ties-overflow", 3, 151936, 1.0, 20, 0.95, True),
+    ("split-smallest-vocab", 3, 16384, 1.0, 20, 0.95, False),
+    ("split-ragged-vocab", 3, 16387, 1.0, 20, 0.95, False),
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_target_filter_parity(case):
+    """Both launch forms (rows split over several workgroups through the workspace, and one
+    workgroup per row) against the oracle, and bit-identical to each other."""
     from paper_2608_05448_amd import dblast as D
     name, N, V, T, k, p, ties = case
     print(f"[target] {name} N={N} V={V} T={T} k={k} p={p}", flush=True)
     lg = _logits(N, V, 7 + len(name), ties)
-    got = D.dbl_target_logprobs(torch.from_numpy(lg).cuda(), T, k, p)
+    lgd = torch.from_numpy(lg).cuda()
+    got = D.dbl_target_logprobs(lgd, T, k, p)
+    one = D.dbl_target_logprobs(lgd, T, k, p, split=False)
     torch.cuda.synchronize()
+    assert torch.equal(got, one)
     got = got.cpu().numpy()
     want = TG.filter_logprobs(lg, T, k, p)
     assert np.array_equal(np.isfinite(got), np.isfinite(want))
@@ -78,16 +88,19 @@ def test_target_filter_benchmark_rows():
     N, V = 272, 151936
     lg = torch.from_numpy(_logits(N, V, 99)).cuda()
     out = torch.empty_like(lg)
+    ws = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_TARGET, N, 1, 1, 0, V), dtype=torch.uint8,
+                     device="cuda")
     for T, k, p in ((0.7, 20, 0.8), (1.0, 20, 0.95), (1.5, 20, 1.0), (1.0, 0, 0.95)):
-        D.dbl_target_logprobs(lg, T, k, p, out=out)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(5):
-            D.dbl_target_logprobs(lg, T, k, p, out=out)
-        torch.cuda.synchronize()
-        ms = (time.perf_counter() - t0) / 5 * 1e3
-        print(f"[target] rows {N} x {V}, T={T} k={k} p={p}: {ms:.3f} ms "
-              f"({N * V * 8 / ms / 1e6:.0f} GB/s of logits in + logp out)", flush=True)
+        for split in (True, False):
+            D.dbl_target_logprobs(lg, T, k, p, out=out, ws=ws, split=split)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(5):
+                D.dbl_target_logprobs(lg, T, k, p, out=out, ws=ws, split=split)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) / 5 * 1e3
+            print(f"[target] rows {N} x {V}, T={T} k={k} p={p} split={split}: {ms:.3f} ms "
+                  f"({N * V * 8 / ms / 1e6:.0f} GB/s of logits in + logp out)", flush=True)
     rows = [0, 135, 271]
     want = TG.filter_logprobs(lg[rows].cpu().numpy(), 1.0, 0, 0.95)
     got = out[rows].cpu().numpy()
