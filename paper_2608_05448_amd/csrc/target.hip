@@ -188,6 +188,32 @@ constexpr int kCandCap = 4096;
 // lower bound of the row's k-th largest s - in visiting order (s descending, id ascending),
 // applies both cuts and writes the kept tokens' log-probabilities; the rest of the output row
 // already holds -inf. Needs n >= k and n <= kCandCap; all kFT threads call it.
+// Sorts cand[0, n) (n <= kCandCap) in descending order: a bitonic network over the list padded
+// with zeros to a power of two (every visiting key has a nonzero low word, ids being below
+// 2^32 - 1). All kFT threads call it; it ends with a barrier.
+__device__ void block_sort_desc(uint64_t* cand, int n) {
+  const int tid = threadIdx.x;
+  int np = 64;
+  while (np < n) np <<= 1;
+  for (int i = n + tid; i < np; i += kFT) cand[i] = 0;
+  __syncthreads();
+  for (int size = 2; size <= np; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < (np >> 1); i += kFT) {
+        const int i0 = 2 * i - (i & (stride - 1));  // the pair (i0, i0 + stride)
+        const int i1 = i0 + stride;
+        const bool desc = (i0 & size) == 0;
+        const uint64_t x = cand[i0], y = cand[i1];
+        if ((x < y) == desc) {
+          cand[i0] = y;
+          cand[i1] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
 // Wavefront 0 alone, when the tokens tied with or above the k-th largest s number at most 64
 // (the usual case for small k): those nk tokens are gathered one per lane, sorted in visiting
 // order with a register bitonic network, and both cuts and the normaliser are wavefront
@@ -293,27 +319,7 @@ __device__ void finish_candidates(const FilterArgs& a, float* out, uint64_t* can
     if (tid < 64) finish_small(a, out, cand, n, tk0, nk0);
     return;
   }
-  // bitonic sort, descending, of the list padded with zeros to a power of two (every real
-  //    entry has a nonzero low word, ids being below 2^32 - 1)
-  int np = 64;
-  while (np < n) np <<= 1;
-  for (int i = n + tid; i < np; i += kFT) cand[i] = 0;
-  __syncthreads();
-  for (int size = 2; size <= np; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < (np >> 1); i += kFT) {
-        const int i0 = 2 * i - (i & (stride - 1));  // the pair (i0, i0 + stride)
-        const int i1 = i0 + stride;
-        const bool desc = (i0 & size) == 0;
-        const uint64_t x = cand[i0], y = cand[i1];
-        if ((x < y) == desc) {
-          cand[i0] = y;
-          cand[i1] = x;
-        }
-      }
-      __syncthreads();
-    }
-  }
+  block_sort_desc(cand, n);
   auto key_at = [&](int i) { return static_cast<uint32_t>(cand[i] >> 32); };
   const float m = key_value(key_at(0));
   // top-k: the first k entries and every later one tied with the k-th (n >= k: the list holds
@@ -648,6 +654,127 @@ __device__ void filter_general(const FilterArgs& a, const float* in, float* out,
   });
 }
 
+// Nucleus alone (top_k off, p < 1): with m the row maximum, every token's integer mass
+// P(v) = floor(detexp32(fl32(s - m)) 2^40) goes to one of kNucBins bins by
+// floor((m - s) kNucScale), which is non-increasing in s, so bins are ordered like s and tokens
+// of one bin are contiguous in visiting order. The bin where the running mass reaches
+// T_p = ceil(p Z) is the only one whose tokens need ordering: they are gathered and sorted, and
+// the cut is found in it. Tokens with P = 0 follow all positive masses, whose total Z >= T_p, so
+// they are never kept. The normaliser is the kept integer mass times 2^-40, within 2^-40 per
+// token plus detexp32's rounding of the binary64 sum of exp(s - m). Four reads and one write of
+// the row. Returns false (nothing written) if the cut's bin holds more than kCandCap tokens.
+constexpr int kNucBins = 2048;
+constexpr float kNucScale = kNucBins / 27.8f;  // P(v) = 0 below s - m = -40 ln 2 = -27.73
+
+__device__ bool filter_nucleus(const FilterArgs& a, const float* in, float* out, bool vec,
+                               uint64_t* bins, uint64_t* cand, uint64_t* red, int* sh_n) {
+  const int tid = threadIdx.x;
+  const int64_t V = a.V;
+  const float T = a.temperature;
+  // 1. maximum (division by T is monotone: the largest s is that of the largest logit)
+  uint32_t mk = 0;
+  row_scan_raw<4>(in, V, vec, [&](int64_t, float lv) {
+    const uint32_t x = order_key(lv);
+    mk = x > mk ? x : mk;
+  });
+  const float m = __fdiv_rn(key_value(static_cast<uint32_t>(block_max_u64(mk, red))), T);
+  auto mass_bin = [&](float sv, uint64_t* P) {
+    const float d = __fsub_rn(sv, m);
+    *P = quant40(detexp32(d));
+    return min(kNucBins - 1, static_cast<int>(__fmul_rn(-d, kNucScale)));
+  };
+  // 2. integer mass per bin
+  for (int i = tid; i < kNucBins; i += kFT) bins[i] = 0;
+  __syncthreads();
+  row_scan<2>(in, V, T, vec, [&](int64_t, float sv) {
+    uint64_t P;
+    const int b = mass_bin(sv, &P);
+    if (P) atomicAdd(reinterpret_cast<unsigned long long*>(&bins[b]), static_cast<unsigned long long>(P));
+  });
+  __syncthreads();
+  // the crossing bin: exclusive prefix of the bin masses (two bins per thread)
+  const uint64_t b0 = bins[2 * tid], b1 = bins[2 * tid + 1];
+  const uint64_t loc = b0 + b1;
+  const uint64_t incl = wave_incl_scan_u64(loc);
+  if (lane_id() == 63) red[tid >> 6] = incl;
+  __syncthreads();
+  uint64_t base = 0, z = 0;
+#pragma unroll
+  for (int w = 0; w < kFW; ++w) {
+    const uint64_t r = red[w];
+    base += w < (tid >> 6) ? r : 0;
+    z += r;
+  }
+  __syncthreads();
+  uint64_t tp = static_cast<uint64_t>(ceil(__dmul_rn(static_cast<double>(a.top_p),
+                                                     static_cast<double>(z))));
+  if (tp == 0) tp = 1;
+  const uint64_t ex0 = base + incl - loc, ex1 = ex0 + b0;  // mass before bins 2 tid, 2 tid + 1
+  if (ex0 < tp && tp <= ex1) {
+    red[0] = 2 * tid;
+    red[1] = ex0;
+  } else if (ex1 < tp && tp <= ex1 + b1) {
+    red[0] = 2 * tid + 1;
+    red[1] = ex1;
+  }
+  if (tid == 0) *sh_n = 0;
+  __syncthreads();
+  const int bstar = static_cast<int>(red[0]);
+  const uint64_t before = red[1];
+  __syncthreads();
+  // 3. the crossing bin's tokens, then their order
+  row_scan<2>(in, V, T, vec, [&](int64_t v, float sv) {
+    uint64_t P;
+    if (mass_bin(sv, &P) == bstar && P) {
+      const int slot = atomicAdd(sh_n, 1);
+      if (slot < kCandCap) cand[slot] = visit_key(order_key(sv), v);
+    }
+  });
+  __syncthreads();
+  const int n = *sh_n;
+  __syncthreads();
+  if (n > kCandCap) return false;
+  block_sort_desc(cand, n);
+  // kept prefix of the bin: four entries per thread in visiting order
+  uint64_t P4[4], l4 = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = 4 * tid + j;
+    P4[j] = i < n ? quant40(detexp32(__fsub_rn(key_value(static_cast<uint32_t>(cand[i] >> 32)), m))) : 0;
+    l4 += P4[j];
+  }
+  const uint64_t inc4 = wave_incl_scan_u64(l4);
+  if (lane_id() == 63) red[tid >> 6] = inc4;
+  __syncthreads();
+  uint64_t base4 = 0;
+#pragma unroll
+  for (int w = 0; w < kFW; ++w) base4 += w < (tid >> 6) ? red[w] : 0;
+  __syncthreads();
+  uint64_t run = before + base4 + inc4 - l4;
+  uint64_t cnt = 0, kept_mass = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (4 * tid + j < n && run < tp) {
+      ++cnt;
+      kept_mass += P4[j];
+    }
+    run += P4[j];
+  }
+  const uint64_t nkeep = block_sum_u64(cnt, red);
+  const uint64_t kmass = before + block_sum_u64(kept_mass, red);
+  const uint64_t cut = cand[nkeep - 1];
+  const double lse = log(static_cast<double>(kmass)) - 40.0 * 0.6931471805599453;
+  // 4. output row
+  row_scan<2>(in, V, T, vec, [&](int64_t v, float sv) {
+    uint64_t P;
+    const int b = mass_bin(sv, &P);
+    const bool kept = P && (b < bstar || (b == bstar && visit_key(order_key(sv), v) >= cut));
+    out[v] = kept ? static_cast<float>(static_cast<double>(sv) - static_cast<double>(m) - lse)
+                  : -INFINITY;
+  });
+  return true;
+}
+
 __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
   __shared__ uint64_t hist[256];
   __shared__ uint64_t cand[kCandCap];
@@ -681,6 +808,27 @@ __global__ __launch_bounds__(kFT) void filter_kernel(FilterArgs a) {
       filter_fast(a, in, out, vec, cand, resc, red, redd, &sh_n, &sh_r))
     return;
 
+  filter_general(a, in, out, vec, hist, red, redd, &sh_digit, &sh_above);
+}
+
+// Rows with the nucleus alone (T > 0, top_k off, p < 1): the binned path, or the general one
+// when the cut's bin is too crowded.
+__global__ __launch_bounds__(kFT) void filter_nucleus_kernel(FilterArgs a) {
+  __shared__ uint64_t hist[256];
+  __shared__ uint64_t nbins[kNucBins];
+  __shared__ uint64_t cand[kCandCap];
+  __shared__ int sh_n;
+  __shared__ uint64_t red[kFW];
+  __shared__ double redd[kFW];
+  __shared__ uint32_t sh_digit;
+  __shared__ uint64_t sh_above;
+  const int64_t n = blockIdx.x;
+  const int64_t V = a.V;
+  const float* in = a.logits + n * V;
+  float* out = a.logp + n * V;
+  const bool vec = (V & 3) == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  if (filter_nucleus(a, in, out, vec, nbins, cand, red, &sh_n)) return;
   filter_general(a, in, out, vec, hist, red, redd, &sh_digit, &sh_above);
 }
 
@@ -872,6 +1020,13 @@ hipError_t launch_filter(const FilterArgs& a, hipStream_t stream) {
   if (a.N > 0x7fffffff / kFilterSegs) return hipErrorInvalidConfiguration;
   const bool split = a.seg_cand && a.seg_count && a.temperature > 0.0f && a.top_k > 0 &&
                      a.top_k <= 256 && a.top_k < a.V && a.V >= kFilterSegs * 4096;
+  const bool nucleus = a.temperature > 0.0f && (a.top_k == 0 || a.top_k >= a.V) &&
+                       a.top_p < 1.0f;
+  if (nucleus) {
+    hipLaunchKernelGGL(filter_nucleus_kernel, dim3(static_cast<unsigned>(a.N)), dim3(kFT), 0,
+                       stream, a);
+    return hipGetLastError();
+  }
   if (!split) {
     hipLaunchKernelGGL(filter_kernel, dim3(static_cast<unsigned>(a.N)), dim3(kFT), 0, stream, a);
     return hipGetLastError();

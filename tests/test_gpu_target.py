@@ -58,6 +58,12 @@ CASES = [
     ("split-ties-overflow", 3, 151936, 1.0, 20, 0.95, True),
     ("split-smallest-vocab", 3, 16384, 1.0, 20, 0.95, False),
     ("split-ragged-vocab", 3, 16387, 1.0, 20, 0.95, False),
+    ("nucleus-p0999", 3, 151936, 1.0, 0, 0.999, False),
+    ("nucleus-p001", 3, 151936, 1.0, 0, 0.01, False),
+    ("nucleus-high-T", 3, 151936, 5.0, 0, 0.9, False),
+    ("nucleus-top-k-ge-V", 2, 3000, 1.0, 5000, 0.8, False),
+    ("nucleus-ragged-vocab", 3, 50001, 0.7, 0, 0.8, False),
+    ("flat-row-nucleus", 2, 151936, 1.0, 0, 0.95, "flat"),
 ]
 
 
