@@ -665,6 +665,185 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
         acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w, m0 + wm * C::TM, lane, ea.vec4);
 }
 
+
+// ---------------------------------------------------------------------------------------
+// Register-staged variant (hidden sizes that are a multiple of 64): 64-deep stages, so every
+// 128-byte row segment of a stage is one request, and a lead of two stages for every load.
+// The LDS holds two stages (128 KB); two more stages are in flight in registers (16 16-byte
+// loads per thread per stage): during stage kt the threads write stage kt + 1 from registers
+// to the LDS slot stage kt - 1 has left and refill those registers with stage kt + 3. The main
+// loop needs few VGPRs besides the staging ones (the accumulators are in AGPRs), so the staging
+// costs no occupancy. One barrier per stage, before its last k step; the same 128 x 128 wave
+// tiles, fragment order and epilogues as the direct-to-LDS kernel.
+namespace rs {
+constexpr int BV = 256, BM = 256, BK = 64, WM = 2, NW = 4, kThreads = 256;
+constexpr int TM = BM / WM, NCB = TM / 32, NRB = 4;
+constexpr int CPR = BK / 8, ROWB = BK * 2;        // 8 chunks of 16 bytes per 128-byte row
+constexpr int TILE = BV * ROWB;                    // bytes of one operand tile of a stage
+constexpr int LD = BV * CPR / kThreads;            // 16-byte loads per thread per operand (8)
+constexpr int KS = BK / 16;                        // k steps per stage (4)
+#ifndef DBL_RS_SPREAD
+#define DBL_RS_SPREAD 2
+#endif
+constexpr int kSpread = DBL_RS_SPREAD;             // k steps carrying the staging traffic
+static_assert(BV == BM, "both operands use the same load mapping");
+static_assert(kSpread >= 1 && kSpread <= KS - 1, "staging ends before the stage's barrier");
+}  // namespace rs
+
+template <int EPI>
+__global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
+    const __bf16* __restrict__ h, const __bf16* __restrict__ w, const EpiArgs ea, int64_t M,
+    int64_t V, int d, int n_mtiles) {
+  using namespace rs;
+  __shared__ __attribute__((aligned(1024))) char sA0[TILE], sB0[TILE], sA1[TILE], sB1[TILE];
+  char* const sA[2] = {sA0, sA1};
+  char* const sB[2] = {sB0, sB1};
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wv = wave / WM;
+  const int wm = wave % WM;
+  int vt, mt;
+  tile_of(xcd_remap(blockIdx.x, gridDim.x), gridDim.x / n_mtiles, n_mtiles, &vt, &mt);
+  const int64_t v0 = static_cast<int64_t>(vt) * BV;
+  const int64_t m0 = static_cast<int64_t>(mt) * BM;
+
+  // Load i of a thread: tile row 32 i + tid / 8, chunk tid % 8 (eight lanes cover a row's 128
+  // bytes); stored at chunk c ^ swz(row), swz(row) = (row / 2) % 8, which depends only on
+  // tid / 8 here (32 i leaves it unchanged). Rows past V or M are clamped.
+  const char* a_tile = reinterpret_cast<const char*>(w + v0 * d);
+  const char* b_tile = reinterpret_cast<const char*>(h + m0 * d);
+  const int c = tid & 7, r0 = tid >> 3;
+  const int lds0 = r0 * ROWB + ((c ^ dma_swz<CPR>(r0)) * 16);
+  uint32_t a_off[LD], b_off[LD];
+#pragma unroll
+  for (int i = 0; i < LD; ++i) {
+    const int r = 32 * i + r0;
+    const int64_t gv = v0 + r < V ? r : V - 1 - v0;
+    const int64_t gm = m0 + r < M ? r : M - 1 - m0;
+    a_off[i] = static_cast<uint32_t>(gv * d * 2 + c * 16);
+    b_off[i] = static_cast<uint32_t>(gm * d * 2 + c * 16);
+  }
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 ra[2][LD], rb[2][LD];
+
+  f32x16 acc[NRB][NCB];
+#pragma unroll
+  for (int rb_ = 0; rb_ < NRB; ++rb_)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[rb_][cb][r] = 0.0f;
+
+  const int tt = 16 * ((lane >> 5) ^ dma_swz<CPR>(lane & 31));
+  const int a_base = (wv * kVTile + (lane & 31)) * ROWB;
+  const int b_base = (wm * TM + (lane & 31)) * ROWB;
+  bf16x8 af[2][NRB], bfr[2][NCB];
+  auto load_frag = [&](int set, const char* As, const char* Bs, int ks, int i) {
+    const int x = (32 * ks) ^ tt;
+    if (i < NRB)
+      af[set][i] = *reinterpret_cast<const bf16x8*>(As + a_base + i * 32 * ROWB + x);
+    else
+      bfr[set][i - NRB] = *reinterpret_cast<const bf16x8*>(Bs + b_base + (i - NRB) * 32 * ROWB + x);
+  };
+  auto mfma = [&](int set, int q) {
+    const int rb_ = q / NCB, cb = q % NCB;
+    acc[rb_][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[set][rb_], bfr[set][cb],
+                                                            acc[rb_][cb], 0, 0, 0);
+  };
+  const int nk = d / BK;
+  // global -> registers (stage s, clamped to the last stage) and registers -> LDS, one 16-byte
+  // load of one operand at a time (q < LD: w, else h)
+  auto gload = [&](auto buf_c, int s, int q) {
+    constexpr int buf = decltype(buf_c)::value;
+    const int koff = min(s, nk - 1) * ROWB;
+    if (q < LD)
+      ra[buf][q] = *reinterpret_cast<const u32x4*>(a_tile + a_off[q] + koff);
+    else
+      rb[buf][q - LD] = *reinterpret_cast<const u32x4*>(b_tile + b_off[q - LD] + koff);
+  };
+  auto swrite = [&](auto buf_c, auto slot_c, int q) {
+    constexpr int buf = decltype(buf_c)::value, slot = decltype(slot_c)::value;
+    if (q < LD)
+      *reinterpret_cast<u32x4*>(sA[slot] + lds0 + q * 32 * ROWB) = ra[buf][q];
+    else
+      *reinterpret_cast<u32x4*>(sB[slot] + lds0 + (q - LD) * 32 * ROWB) = rb[buf][q - LD];
+  };
+  constexpr int NF = NRB + NCB, NQ = NRB * NCB, NSLOT = NQ / 2;
+  auto frag_of = [](int f) { return f == 0 ? 0 : (f <= NCB ? NRB + f - 1 : f - NCB); };
+
+  // Prologue: stage 0 in LDS slot 0, stage 1 in registers (buffer 1), stage 2 in flight
+  // (buffer 0), stage 0's first fragments loaded.
+#pragma unroll
+  for (int q = 0; q < 2 * LD; ++q) gload(std::integral_constant<int, 0>{}, 0, q);
+#pragma unroll
+  for (int q = 0; q < 2 * LD; ++q) gload(std::integral_constant<int, 1>{}, 1, q);
+#pragma unroll
+  for (int q = 0; q < 2 * LD; ++q) {
+    swrite(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, q);
+    gload(std::integral_constant<int, 0>{}, 2, q);
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int f = 0; f < NF; ++f) load_frag(0, sA[0], sB[0], 0, frag_of(f));
+
+  // Stage kt (slot j = kt % 2): its first two k steps write stage kt + 1 (registers j ^ 1) to
+  // slot j ^ 1 and reload those registers with stage kt + 3; registers j hold stage kt + 2.
+  // Before the last k step: LDS writes done, barrier; the last k step loads stage kt + 1's
+  // first fragments.
+  auto body = [&](auto j_c, int kt) {
+    constexpr int j = decltype(j_c)::value;
+    constexpr int jn = j ^ 1;
+#pragma unroll
+    for (int st = 0; st < KS; ++st) {
+      const int cur = st & 1;
+      if (st == KS - 1) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+      }
+#pragma unroll
+      for (int i = 0; i < NSLOT; ++i) {
+        mfma(cur, 2 * i);
+        mfma(cur, 2 * i + 1);
+        if (st < KS - 1) {
+          load_frag(cur ^ 1, sA[j], sB[j], st + 1, frag_of(i));
+        } else {
+          load_frag(0, sA[jn], sB[jn], 0, frag_of(i));
+        }
+        if (st < kSpread) {
+          constexpr int TS = kSpread * NSLOT;
+          const int g = st * NSLOT + i;
+#pragma unroll
+          for (int q = g * 2 * LD / TS; q < (g + 1) * 2 * LD / TS; ++q) {
+            swrite(std::integral_constant<int, jn>{}, std::integral_constant<int, jn>{}, q);
+            gload(std::integral_constant<int, jn>{}, kt + 3, q);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+  static_assert(NF == NSLOT, "one fragment load per MFMA pair");
+  int kt0 = 0;
+  for (; kt0 + 2 <= nk; kt0 += 2) {
+    body(std::integral_constant<int, 0>{}, kt0);
+    body(std::integral_constant<int, 1>{}, kt0 + 1);
+  }
+  if (kt0 < nk) body(std::integral_constant<int, 0>{}, kt0);
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+
+  const int64_t v0w = v0 + wv * kVTile;
+  if (v0w >= V) return;
+  if constexpr (EPI == kEpiExpand)
+    expand_store<NRB, NCB>(acc, ea, M, V, v0w, m0 + wm * TM, lane);
+  else
+    tile_logsoftmax_store<NRB, NCB, EPI == kEpiLogSoftmaxArgmax>(
+        acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w, m0 + wm * TM, lane, ea.vec4);
+}
+
 // fp32 path: workgroup (vocabulary tile t, 4 branch rows); thread j owns id 128 t + j.
 constexpr int kF32Rows = 4;
 constexpr int kF32DChunk = 512;
@@ -801,7 +980,27 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
     const int vec4 = (a.V % 4 == 0) ? 1 : 0;
     const __bf16* h = static_cast<const __bf16*>(a.h);
     const __bf16* w = static_cast<const __bf16*>(a.w);
-    if (a.d % DCfg::BK == 0) {
+#ifndef DBL_HEAD_RS
+#define DBL_HEAD_RS 1
+#endif
+    if (DBL_HEAD_RS && a.d % rs::BK == 0) {
+      const int dm = static_cast<int>((a.M + rs::BM - 1) / rs::BM);
+      const int64_t dwg = ((a.V + rs::BV - 1) / rs::BV) * dm;
+      if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
+      const dim3 grid(static_cast<unsigned>(dwg)), block(rs::kThreads);
+      EpiArgs ea{};
+      ea.tls = a.tls;
+      ea.lmass = a.lmass;
+      ea.amax = amax;
+      ea.nT = nT;
+      ea.vec4 = vec4;
+      if (amax)
+        hipLaunchKernelGGL((head_bf16_rs_kernel<kEpiLogSoftmaxArgmax>), grid, block, 0, stream, h,
+                           w, ea, a.M, a.V, a.d, dm);
+      else
+        hipLaunchKernelGGL((head_bf16_rs_kernel<kEpiLogSoftmax>), grid, block, 0, stream, h, w,
+                           ea, a.M, a.V, a.d, dm);
+    } else if (a.d % DCfg::BK == 0) {
       const int dm = static_cast<int>((a.M + DCfg::BM - 1) / DCfg::BM);
       const int64_t dwg = ((a.V + DCfg::BV - 1) / DCfg::BV) * dm;
       if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
