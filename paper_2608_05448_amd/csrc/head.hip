@@ -69,17 +69,15 @@ __device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], f
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if constexpr (ARG) {
-            if (acc[rb][cb][r] > mx) {
-              mx = acc[rb][cb][r];
-              vi = rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-            }
-          } else {
-            mx = fmaxf(mx, acc[rb][cb][r]);
-          }
-        }
-      if constexpr (ARG) {
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[rb][cb][r]);
+      if constexpr (ARG) {  // this lane's first id holding its maximum (ids rise with rb, r)
+        vi = 1 << 30;
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (acc[rb][cb][r] == mx) vi = min(vi, rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3));
+        vi = vi == (1 << 30) ? 0 : vi;
         const float omx = __shfl_xor(mx, 32);
         const int ovi = __shfl_xor(vi, 32);
         if (omx > mx || (omx == mx && ovi < vi)) {
@@ -100,16 +98,18 @@ __device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], f
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int o = rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          if constexpr (ARG) {
-            if (o < vlim && acc[rb][cb][r] > mx) {
-              mx = acc[rb][cb][r];
-              vi = o;
-            }
-          } else {
-            if (o < vlim) mx = fmaxf(mx, acc[rb][cb][r]);
-          }
+          if (o < vlim) mx = fmaxf(mx, acc[rb][cb][r]);
         }
       if constexpr (ARG) {
+        vi = 1 << 30;
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int o = rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+            if (o < vlim && acc[rb][cb][r] == mx) vi = min(vi, o);
+          }
+        vi = vi == (1 << 30) ? 0 : vi;
         const float omx = __shfl_xor(mx, 32);
         const int ovi = __shfl_xor(vi, 32);
         if (omx > mx || (omx == mx && ovi < vi)) {
