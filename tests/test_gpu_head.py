@@ -64,6 +64,8 @@ def test_head_fp32_ragged(B, K, R, d, V):
     (1, 4, 5, 64, 1001),     # V % 4 != 0: scalar stores
     (1, 1, 5, 8, 77),        # fewer ids than one tile
     (4, 16, 8, 256, 2048),   # exact tile multiples
+    (2, 3, 5, 96, 3001),     # hidden size a multiple of 32 but not 64: direct-to-LDS kernel
+    (1, 16, 8, 192, 4100),   # three 64-deep stages (odd count) in the register-staged kernel
 ])
 def test_head_bf16_ragged(B, K, R, d, V):
     h = synth.make_uniform_logits((B, K, R, d), 21).to(torch.bfloat16)
