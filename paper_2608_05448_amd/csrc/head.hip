@@ -5,7 +5,10 @@
 // vocabulary along the MFMA rows and the branch rows along the MFMA columns, so each lane holds
 // 16 logits of one branch row. The per-tile (128 ids) max and sum of exponentials therefore
 // reduce in registers plus one cross-half exchange, and the tile-normalised log-probs are
-// stored straight from the accumulators: logits never reach memory.
+// stored straight from the accumulators: logits never reach memory. Operand feeds, by hidden
+// size: d % 64 == 0, 64-deep stages staged through registers (the main path); d % 32 == 0,
+// 32-deep stages copied global -> LDS directly (also used by the branch expander); otherwise a
+// register-staged kernel with padded LDS rows.
 //
 // fp32 path: a plain fp32 kernel for fp32 inputs (small problems).
 #include <hip/hip_runtime.h>
@@ -728,7 +731,6 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
     a_off[i] = static_cast<uint32_t>(gv * d * 2 + c * 16);
     b_off[i] = static_cast<uint32_t>(gm * d * 2 + c * 16);
   }
-  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
   u32x4 ra[2][LD], rb[2][LD];
 
   f32x16 acc[NRB][NCB];
