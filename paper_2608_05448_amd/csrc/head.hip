@@ -941,20 +941,20 @@ __global__ __launch_bounds__(256) void lse_finalize_kernel(const float* __restri
   const int lane = threadIdx.x & 63;
   if (m >= M) return;
   const float* row = lmass + m * nT;
-  // Single pass: every lane keeps a running (max, sum of exp relative to max) pair, and the
-  // pairs are merged across the wavefront.
-  float mx = -INFINITY, s = 0.0f;
-  for (int t = lane; t < nT; t += 64) {
-    const float x = row[t];
-    if (x > mx) {
-      s = s * __expf(mx - x) + 1.0f;
-      mx = x;
-    } else if (x > -INFINITY) {
-      s += __expf(x - mx);
+  // Two passes over the row (the second from cache): the maximum, then the sum of exponentials
+  // relative to it; the loads of a pass are independent, so they overlap.
+  float mx = -INFINITY;
+#pragma unroll 4
+  for (int t = lane; t < nT; t += 64) mx = fmaxf(mx, row[t]);
+  const float gmx = wave_max(mx);
+  float s = 0.0f;
+  if (gmx > -INFINITY) {
+#pragma unroll 4
+    for (int t = lane; t < nT; t += 64) {
+      const float x = row[t];
+      s += x > -INFINITY ? __expf(x - gmx) : 0.0f;
     }
   }
-  const float gmx = wave_max(mx);
-  s = mx > -INFINITY ? s * __expf(mx - gmx) : 0.0f;
   s = wave_sum(s);
   if (lane == 0) {
     lse[m] = gmx + __logf(s);
