@@ -137,25 +137,34 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
   }
   if (a.trajectory) return;
   __syncthreads();
-  if (tid == 0) {
-    bool alive = true;
-    int n_acc = 0;
+  // Wavefront 0: 64 positions' accept tests at a time (the draws do not depend on earlier
+  // outcomes); n_accept is the index of the first rejection. The running product of the A_k is
+  // taken in position order by every lane alike.
+  if (wave == 0) {
+    int n_acc = K;
     double prodA = 1.0, al = 0.0;
-    for (int k = 0; k < K; ++k) {
-      const double Q = s_Q[k], P = s_P[k];
-      const double A = Q > 0.0 ? fmin(1.0, P / Q) : (P > 0.0 ? 1.0 : 0.0);
-      prodA = __dmul_rn(prodA, A);
-      al = __dadd_rn(al, prodA);
-      if (alive) {
+    for (int k0 = 0; k0 < K; k0 += 64) {
+      const int k = k0 + lane;
+      bool rej = false;
+      double A = 0.0;
+      if (k < K) {
+        const double Q = s_Q[k], P = s_P[k];
+        A = Q > 0.0 ? fmin(1.0, P / Q) : (P > 0.0 ? 1.0 : 0.0);
         const uint32_t r = draw(k_.seed, kAccept, static_cast<uint32_t>(k), seq, k_.step);
-        if (accept_int(r, quant40d(Q), quant40d(P)))
-          ++n_acc;
-        else
-          alive = false;
+        rej = !accept_int(r, quant40d(Q), quant40d(P));
+      }
+      const uint64_t rejm = __ballot(rej);
+      if (rejm && n_acc == K) n_acc = k0 + __ffsll(static_cast<unsigned long long>(rejm)) - 1;
+      const int kn = min(64, K - k0);
+      for (int j = 0; j < kn; ++j) {
+        prodA = __dmul_rn(prodA, __shfl(A, j));
+        al = __dadd_rn(al, prodA);
       }
     }
-    a.n_accept[b] = n_acc;
-    if (a.al) a.al[b] = static_cast<float>(al);
+    if (lane == 0) {
+      a.n_accept[b] = n_acc;
+      if (a.al) a.al[b] = static_cast<float>(al);
+    }
   }
 }
 
