@@ -164,6 +164,127 @@ __device__ __forceinline__ void tile_logsoftmax_store(f32x16 (&acc)[NRB][NCB], f
   }
 }
 
+// Epilogue of the register-staged kernel: the same results as tile_logsoftmax_store, with
+// the stores routed through a 16 KB LDS scratch per wave (xp). In the register layout a
+// 16-byte store instruction covers 32 rows, 32 bytes each; every row of tls is V * 4 bytes from
+// the next, so each such instruction needs tens of address translations, which the vector L1
+// serialises. Here the wave writes its 32 rows x 128 ids to LDS as 512-byte rows (16-byte chunk
+// c of row r at chunk c ^ (r % 16): conflict-free both ways) and reads them back so that each
+// store instruction writes two whole 512-byte row segments. One block of 32 rows at a time:
+// its 64 logits per lane are copied out of the accumulators once; in the vocabulary's last,
+// partial tile the ids past V are set to -inf first, so every tile takes the same arithmetic.
+template <int NRB, int NCB, bool ARG>
+__device__ __forceinline__ void tile_logsoftmax_store_lds(f32x16 (&acc)[NRB][NCB], float* tls,
+                                                          float* lmass, uint64_t* amax,
+                                                          int64_t M, int64_t V, int nT,
+                                                          int64_t v0w, int64_t m0w, int lane,
+                                                          int vec4, char* xp) {
+  const int half = lane >> 5;
+  const int lr = lane & 31;
+  const int t = static_cast<int>(v0w / kVTile);
+  const int vlim = static_cast<int>(V - v0w < kVTile ? V - v0w : kVTile);  // ids in this tile
+  const bool full = vlim == kVTile;
+  constexpr int NX = NRB * 16;
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    __builtin_amdgcn_sched_barrier(0);
+    const int64_t m = m0w + cb * 32 + lr;
+    float x[NX];  // x[16 rb + r]: id 32 rb + 8 (r / 4) + 4 half + r % 4 of the tile
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[16 * rb + r] = acc[rb][cb][r];
+    if (!full) {
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3) >= vlim) x[16 * rb + r] = -INFINITY;
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NX; ++i) mx = fmaxf(mx, x[i]);
+    int vi = 0;  // offset in the tile of this lane's first maximum (ARG only)
+    if constexpr (ARG) {
+      vi = 1 << 30;
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (x[16 * rb + r] == mx) vi = min(vi, rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3));
+      vi = vi == (1 << 30) ? 0 : vi;
+      const float omx = __shfl_xor(mx, 32);
+      const int ovi = __shfl_xor(vi, 32);
+      if (omx > mx || (omx == mx && ovi < vi)) {
+        mx = omx;
+        vi = ovi;
+      }
+    } else {
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+    }
+    const float nb = -mx * kLog2e;
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NX; ++i) s += __builtin_amdgcn_exp2f(fmaf(x[i], kLog2e, nb));
+    s += __shfl_xor(s, 32);
+    const float lm = mx + __logf(s);
+    if (m < M && half == 0) {
+      lmass[m * nT + t] = lm;
+      if constexpr (ARG)
+        atomicMax(reinterpret_cast<unsigned long long*>(amax + m),
+                  static_cast<unsigned long long>(argmax_key(mx, v0w + vi)));
+    }
+    float* const base = tls + (m0w + cb * 32) * V + v0w;  // wave-uniform
+    const bool fast = full && vec4 && m0w + cb * 32 + 32 <= M && V < (int64_t{1} << 25);
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float4 o;
+        o.x = x[16 * rb + 4 * g + 0] - lm;
+        o.y = x[16 * rb + 4 * g + 1] - lm;
+        o.z = x[16 * rb + 4 * g + 2] - lm;
+        o.w = x[16 * rb + 4 * g + 3] - lm;
+        const int chunk = (rb * 8 + 2 * g + half) ^ (lr & 15);
+        *reinterpret_cast<float4*>(xp + lr * 512 + chunk * 16) = o;
+      }
+    // Wave-private LDS region: the writes above precede these reads in the wave's LDS queue.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    float4 o[16];  // o[jj]: ids 4 lr .. 4 lr + 3 of block row 2 jj + half
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) {
+      const int rr = 2 * jj + half;
+      o[jj] = *reinterpret_cast<const float4*>(xp + rr * 512 + ((lr ^ (rr & 15)) * 16));
+    }
+    if (fast) {
+      const uint32_t lo = static_cast<uint32_t>(half * V + 4 * lr);  // 32-bit lane offsets
+      const uint32_t step = static_cast<uint32_t>(2 * V);
+#pragma unroll
+      for (int jj = 0; jj < 16; ++jj)
+        *reinterpret_cast<float4*>(base + (lo + jj * step)) = o[jj];
+    } else {
+#pragma unroll
+      for (int jj = 0; jj < 16; ++jj) {
+        const int rr = 2 * jj + half;
+        if (m0w + cb * 32 + rr < M) {
+          float* q = base + rr * V + 4 * lr;
+          if (vec4 && 4 * lr + 3 < vlim) {
+            *reinterpret_cast<float4*>(q) = o[jj];
+          } else {
+            if (4 * lr + 0 < vlim) q[0] = o[jj].x;
+            if (4 * lr + 1 < vlim) q[1] = o[jj].y;
+            if (4 * lr + 2 < vlim) q[2] = o[jj].z;
+            if (4 * lr + 3 < vlim) q[3] = o[jj].w;
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
 // Tile configuration of the bf16 head kernel.
 //   BV x BM   vocabulary rows x branch rows per workgroup
 //   BK        hidden-dimension slice staged in LDS per step (double-buffered)
@@ -411,6 +532,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+#ifndef DBL_HEAD_XP
+#define DBL_HEAD_XP 1
+#endif
 #ifndef DBL_HEAD_BK
 #define DBL_HEAD_BK 32
 #endif
@@ -841,10 +965,25 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
   if (kt0 < nk) body(std::integral_constant<int, 0>{}, kt0);
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
 
+  // Keep the accumulators in AGPRs past the loop's exit (otherwise all of them are copied to
+  // VGPRs right here, leaving the epilogue no registers to work in).
+#pragma unroll
+  for (int rb_ = 0; rb_ < NRB; ++rb_)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) asm volatile("" : "+a"(acc[rb_][cb]));
+
+  // The last stage's slot is free once every wave has passed that stage's barrier (its reads
+  // came before it; the last k step reads the other slot): 16 KB of it per wave for the stores.
+  const int jl = (nk - 1) & 1;
+  char* const xp = (jl ? (wave < 2 ? sA1 : sB1) : (wave < 2 ? sA0 : sB0)) + (wave & 1) * (TILE / 2);
+  static_assert(TILE / 2 >= 32 * 512, "16 KB of LDS per wave for the transposed stores");
   const int64_t v0w = v0 + wv * kVTile;
   if (v0w >= V) return;
   if constexpr (EPI == kEpiExpand)
     expand_store<NRB, NCB>(acc, ea, M, V, v0w, m0 + wm * TM, lane);
+  else if constexpr (DBL_HEAD_XP)
+    tile_logsoftmax_store_lds<NRB, NCB, EPI == kEpiLogSoftmaxArgmax>(
+        acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w, m0 + wm * TM, lane, ea.vec4, xp);
   else
     tile_logsoftmax_store<NRB, NCB, EPI == kEpiLogSoftmaxArgmax>(
         acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w, m0 + wm * TM, lane, ea.vec4);
