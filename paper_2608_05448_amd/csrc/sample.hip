@@ -24,7 +24,15 @@ __global__ __launch_bounds__(256) void sample_tiles_kernel(SampleArgs a) {
   const int64_t pos = blockIdx.x;
   const int64_t b = pos / k_.K;
   const int64_t k = pos % k_.K;
-  const int z = draw_category(k_, b);
+  // The block's category: drawn by wavefront 0 alone (every workgroup of the block draws the
+  // same one) and shared through LDS.
+  __shared__ int s_z;
+  if (threadIdx.x < 64) {
+    const int zz = draw_category(k_, b);
+    if (threadIdx.x == 0) s_z = zz;
+  }
+  __syncthreads();
+  const int z = s_z;
   if (blockIdx.y == 0 && k == 0 && threadIdx.x == 0) a.z_out[b] = z;
   const int sub = threadIdx.x & 7;                     // lane within the tile's group of 8
   const int t = blockIdx.y * kTilesPerChunk + (threadIdx.x >> 3);

@@ -11,6 +11,20 @@ namespace dbl {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// Value of lane l (wave-uniform l) in every lane: v_readlane on each 32-bit half, a few cycles
+// instead of an LDS-crossbar shuffle.
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
+  const uint32_t lo = static_cast<uint32_t>(
+      __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v)), l));
+  const uint32_t hi = static_cast<uint32_t>(
+      __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v >> 32)), l));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+__device__ __forceinline__ double lane_f64(double v, int l) {
+  return __longlong_as_double(
+      static_cast<long long>(lane_u64(static_cast<uint64_t>(__double_as_longlong(v)), l)));
+}
+
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -65,11 +79,12 @@ __device__ __forceinline__ double prior_log_weight(const float* prior_row, int R
 // addition rounded separately; every lane computes the identical sum. An all -inf row (an
 // impossible prefix) gives all-zero weights.
 __device__ __forceinline__ double normalize_weight(double L, int R) {
-  const double mx = wave_max_f64(L);
+  double mx = lane_f64(L, 0);
+  for (int z = 1; z < R; ++z) mx = fmax(mx, lane_f64(L, z));
   if (!(mx > -INFINITY)) return 0.0;
   const double e = dexp64(__dsub_rn(L, mx));
   double S = 0.0;
-  for (int z = 0; z < R; ++z) S = __dadd_rn(S, __shfl(e, z));
+  for (int z = 0; z < R; ++z) S = __dadd_rn(S, lane_f64(e, z));
   return e / S;
 }
 
@@ -80,13 +95,13 @@ __device__ __forceinline__ int draw_category(const BlockArgs& a, int64_t b) {
   const double w = normalize_weight(prior_log_weight(a.prior + b * a.R, R, a.z_temp), R);
   const uint64_t qz = lane < R ? quant40d(w) : 0;
   uint64_t Z = 0;
-  for (int z = 0; z < R; ++z) Z += __shfl(qz, z);
+  for (int z = 0; z < R; ++z) Z += lane_u64(qz, z);
   if (Z == 0) return -1;
   const uint32_t r = draw(a.seed, kCategory, 0, static_cast<uint64_t>(a.seq_offset + b), a.step);
   const uint64_t T = icdf_threshold(r, Z);
   uint64_t cum = 0;
   for (int z = 0; z < R; ++z) {
-    cum += __shfl(qz, z);
+    cum += lane_u64(qz, z);
     if (cum > T) return z;
   }
   return R - 1;  // unreachable: cum reaches Z > T
