@@ -814,11 +814,17 @@ constexpr int TILE = BV * ROWB;                    // bytes of one operand tile 
 constexpr int LD = BV * CPR / kThreads;            // 16-byte loads per thread per operand (8)
 constexpr int KS = BK / 16;                        // k steps per stage (4)
 #ifndef DBL_RS_SPREAD
-#define DBL_RS_SPREAD 2
+#define DBL_RS_SPREAD 3
 #endif
 constexpr int kSpread = DBL_RS_SPREAD;             // k steps carrying the staging traffic
+#ifndef DBL_RS_LSHIFT
+#define DBL_RS_LSHIFT 4
+#endif
+constexpr int kShift = DBL_RS_LSHIFT;              // slots between a register's LDS write and reload
 static_assert(BV == BM, "both operands use the same load mapping");
 static_assert(kSpread >= 1 && kSpread <= KS - 1, "staging ends before the stage's barrier");
+static_assert(kShift >= 0 && kShift + kSpread * (NRB * NCB / 2) <= KS * (NRB * NCB / 2),
+              "every reload issued within the stage");
 }  // namespace rs
 
 template <int EPI>
@@ -919,10 +925,10 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
 #pragma unroll
   for (int f = 0; f < NF; ++f) load_frag(0, sA[0], sB[0], 0, frag_of(f));
 
-  // Stage kt (slot j = kt % 2): its first two k steps write stage kt + 1 (registers j ^ 1) to
-  // slot j ^ 1 and reload those registers with stage kt + 3; registers j hold stage kt + 2.
-  // Before the last k step: LDS writes done, barrier; the last k step loads stage kt + 1's
-  // first fragments.
+  // Stage kt (slot j = kt % 2): its first kSpread k steps write stage kt + 1 (registers j ^ 1)
+  // to slot j ^ 1, and each of those registers is reloaded with stage kt + 3 kShift MFMA pairs
+  // after its write; registers j hold stage kt + 2. Before the last k step: LDS writes done,
+  // barrier; the last k step loads stage kt + 1's first fragments.
   auto body = [&](auto j_c, int kt) {
     constexpr int j = decltype(j_c)::value;
     constexpr int jn = j ^ 1;
@@ -943,13 +949,21 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
         } else {
           load_frag(0, sA[jn], sB[jn], 0, frag_of(i));
         }
-        if (st < kSpread) {
+        {
+          // Register q is written to LDS at slot q TS / 2LD of the first kSpread k steps and
+          // reloaded kShift slots later.
           constexpr int TS = kSpread * NSLOT;
           const int g = st * NSLOT + i;
+          if (st < kSpread) {
 #pragma unroll
-          for (int q = g * 2 * LD / TS; q < (g + 1) * 2 * LD / TS; ++q) {
-            swrite(std::integral_constant<int, jn>{}, std::integral_constant<int, jn>{}, q);
-            gload(std::integral_constant<int, jn>{}, kt + 3, q);
+            for (int q = g * 2 * LD / TS; q < (g + 1) * 2 * LD / TS; ++q)
+              swrite(std::integral_constant<int, jn>{}, std::integral_constant<int, jn>{}, q);
+          }
+          const int gl = g - kShift;
+          if (gl >= 0 && gl < TS) {
+#pragma unroll
+            for (int q = gl * 2 * LD / TS; q < (gl + 1) * 2 * LD / TS; ++q)
+              gload(std::integral_constant<int, jn>{}, kt + 3, q);
           }
         }
         __builtin_amdgcn_sched_barrier(0);
