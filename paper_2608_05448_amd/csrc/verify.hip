@@ -52,7 +52,7 @@ __global__ __launch_bounds__(64) void chain_kernel(VerifyArgs a) {
     if (a.trajectory) continue;
     const double y = static_cast<double>(detexp32(lq));
     double Q = 0.0;
-    for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, __dmul_rn(__shfl(w, z), __shfl(y, z)));
+    for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, __dmul_rn(lane_f64(w, z), lane_f64(y, z)));
     const double P = ok ? static_cast<double>(detexp32(a.logp[(b * a.Kp + k) * k_.V + xk])) : 0.0;
     const double A = Q > 0.0 ? fmin(1.0, P / Q) : (P > 0.0 ? 1.0 : 0.0);
     prodA = __dmul_rn(prodA, A);
@@ -131,7 +131,7 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
     if (!a.trajectory) {
       const double y = lane < R ? static_cast<double>(detexp32(s_lq[k * R + lane])) : 0.0;
       double Q = 0.0;
-      for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, __dmul_rn(__shfl(w, z), __shfl(y, z)));
+      for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, __dmul_rn(lane_f64(w, z), lane_f64(y, z)));
       if (lane == 0) s_Q[k] = Q;
     }
   }
@@ -157,7 +157,7 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
       if (rejm && n_acc == K) n_acc = k0 + __ffsll(static_cast<unsigned long long>(rejm)) - 1;
       const int kn = min(64, K - k0);
       for (int j = 0; j < kn; ++j) {
-        prodA = __dmul_rn(prodA, __shfl(A, j));
+        prodA = __dmul_rn(prodA, lane_f64(A, j));
         al = __dadd_rn(al, prodA);
       }
     }
@@ -436,12 +436,25 @@ __global__ __launch_bounds__(256) void finalize_kernel(VerifyArgs a, int nchunk)
   if (a.beta || a.exp_len) {
     for (int k0 = 0; k0 < K; k0 += kChainMaxK) {
       const int kn = min(kChainMaxK, K - k0);
-      for (int kk = wave; kk < kn; kk += 4) {
-        const float* part = a.beta_part + (b * k_.K + k0 + kk) * nchunk;
-        double sum = 0.0;
-        for (int c = lane; c < nchunk; c += 64) sum += static_cast<double>(part[c]);
-        sum = wave_sum_f64(sum);
-        if (lane == 0) s_beta[kk] = sum;
+      // Four positions per wavefront at a time: their loads and reductions overlap (each
+      // position's sum is taken in the same order as one at a time).
+      for (int kk0 = 4 * wave; kk0 < kn; kk0 += 16) {
+        double sum[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          sum[u] = 0.0;
+          if (kk0 + u < kn) {
+            const float* part = a.beta_part + (b * k_.K + k0 + kk0 + u) * nchunk;
+            for (int c = lane; c < nchunk; c += 64) sum[u] += static_cast<double>(part[c]);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) sum[u] = wave_sum_f64(sum[u]);
+        if (lane == 0) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (kk0 + u < kn) s_beta[kk0 + u] = sum[u];
+        }
       }
       __syncthreads();
       for (int kk = tid; kk < kn; kk += blockDim.x)
