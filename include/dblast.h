@@ -60,7 +60,9 @@
  *    dbl_workspace_bytes(op, shape) bytes, 256-byte aligned. Array arguments must be 16-byte
  *    aligned (vector loads and stores; any allocator's base pointer is).
  *  - Streams: work is enqueued on `stream` (a hipStream_t; NULL is the default stream) and the
- *    call returns without waiting. Outputs are valid once the stream reaches that point.
+ *    call returns without waiting. Outputs are valid once the stream reaches that point. No
+ *    call allocates, frees, copies, sets memory or synchronises: workspaces are cleared by
+ *    kernels, so the calls may be captured into a HIP graph and replayed.
  *  - Errors: a non-zero dbl_status is returned before anything is launched when an argument is
  *    invalid; DBL_EHIP reports a failed launch. dbl_last_error() gives a message for the
  *    calling thread's last failure. Data-dependent problems (NaN inputs) are not detected.
