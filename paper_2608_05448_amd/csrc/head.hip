@@ -806,33 +806,50 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
 // loop needs few VGPRs besides the staging ones (the accumulators are in AGPRs), so the staging
 // costs no occupancy. One barrier per stage, before its last k step; the same 128 x 128 wave
 // tiles, fragment order and epilogues as the direct-to-LDS kernel.
-namespace rs {
-constexpr int BV = 256, BM = 256, BK = 64, WM = 2, NW = 4, kThreads = 256;
-constexpr int TM = BM / WM, NCB = TM / 32, NRB = 4;
-constexpr int CPR = BK / 8, ROWB = BK * 2;        // 8 chunks of 16 bytes per 128-byte row
-constexpr int TILE = BV * ROWB;                    // bytes of one operand tile of a stage
-constexpr int LD = BV * CPR / kThreads;            // 16-byte loads per thread per operand (8)
-constexpr int KS = BK / 16;                        // k steps per stage (4)
 #ifndef DBL_RS_SPREAD
 #define DBL_RS_SPREAD 3
 #endif
-constexpr int kSpread = DBL_RS_SPREAD;             // k steps carrying the staging traffic
 #ifndef DBL_RS_LSHIFT
 #define DBL_RS_LSHIFT 4
 #endif
-constexpr int kShift = DBL_RS_LSHIFT;              // slots between a register's LDS write and reload
-static_assert(BV == BM, "both operands use the same load mapping");
-static_assert(kSpread >= 1 && kSpread <= KS - 1, "staging ends before the stage's barrier");
-static_assert(kShift >= 0 && kShift + kSpread * (NRB * NCB / 2) <= KS * (NRB * NCB / 2),
-              "every reload issued within the stage");
-}  // namespace rs
+// Tile configuration of the register-staged kernel: BV vocabulary (or output-feature) rows x
+// BM branch rows per workgroup, WV x WM waves, each wave 128 x (BM / WM); 64-deep stages.
+template <int BV_, int BM_, int WV_, int WM_>
+struct RsCfg {
+  static constexpr int BV = BV_, BM = BM_, WV = WV_, WM = WM_, BK = 64;
+  static constexpr int NW = WV * WM, kThreads = 64 * NW;
+  static constexpr int TM = BM / WM, NCB = TM / 32, NRB = 4;
+  static constexpr int CPR = BK / 8, ROWB = BK * 2;  // 8 chunks of 16 bytes per 128-byte row
+  static constexpr int TILEA = BV * ROWB, TILEB = BM * ROWB;  // bytes per stage and operand
+  static constexpr int LDA = BV * CPR / kThreads;    // 16-byte loads per thread, w operand
+  static constexpr int LDB = BM * CPR / kThreads;    // 16-byte loads per thread, h operand
+  static constexpr int NLD = LDA + LDB;
+  static constexpr int KS = BK / 16;                 // k steps per stage (4)
+  static constexpr int NQ = NRB * NCB, NSLOT = NQ / 2, NF = NRB + NCB;
+  static constexpr int kSpread = DBL_RS_SPREAD;      // k steps carrying the LDS writes
+  static constexpr int kShift = DBL_RS_LSHIFT;       // MFMA pairs between a register's write and reload
+  static_assert(BV == 128 * WV && kThreads == 256, "waves of 128 vocabulary rows, 256 threads");
+  static_assert(LDA >= 1 && LDB >= 1 && BV * CPR % kThreads == 0 && BM * CPR % kThreads == 0,
+                "load mapping");
+  static_assert(kSpread >= 1 && kSpread <= KS - 1, "staging ends before the stage's barrier");
+  static_assert(kShift >= 0 && kShift + kSpread * NSLOT <= KS * NSLOT,
+                "every reload issued within the stage");
+  static_assert(NF <= 2 * NSLOT, "at most two fragment loads per MFMA pair");
+  static_assert(2 * (TILEA + TILEB) <= 160 * 1024, "two stages in LDS");
+};
+using RsHead = RsCfg<256, 256, 2, 2>;   // the head: 256 x 256 tiles
+using RsNarrow = RsCfg<128, 256, 1, 4>; // few branch rows (the expander): 128 x 256 tiles
 
-template <int EPI>
-__global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
+template <class C, int EPI>
+__global__ __launch_bounds__(C::kThreads, 1) void head_bf16_rs_kernel(
     const __bf16* __restrict__ h, const __bf16* __restrict__ w, const EpiArgs ea, int64_t M,
     int64_t V, int d, int n_mtiles) {
-  using namespace rs;
-  __shared__ __attribute__((aligned(1024))) char sA0[TILE], sB0[TILE], sA1[TILE], sB1[TILE];
+  constexpr int BV = C::BV, BM = C::BM, BK = C::BK, WM = C::WM, TM = C::TM, NCB = C::NCB,
+                NRB = C::NRB, CPR = C::CPR, ROWB = C::ROWB, LDA = C::LDA, LDB = C::LDB,
+                NLD = C::NLD, KS = C::KS, NSLOT = C::NSLOT, NF = C::NF,
+                kSpread = C::kSpread, kShift = C::kShift;
+  __shared__ __attribute__((aligned(1024))) char sA0[C::TILEA], sB0[C::TILEB], sA1[C::TILEA],
+      sB1[C::TILEB];
   char* const sA[2] = {sA0, sA1};
   char* const sB[2] = {sB0, sB1};
   const int tid = threadIdx.x;
@@ -852,16 +869,20 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
   const char* b_tile = reinterpret_cast<const char*>(h + m0 * d);
   const int c = tid & 7, r0 = tid >> 3;
   const int lds0 = r0 * ROWB + ((c ^ dma_swz<CPR>(r0)) * 16);
-  uint32_t a_off[LD], b_off[LD];
+  uint32_t a_off[LDA], b_off[LDB];
 #pragma unroll
-  for (int i = 0; i < LD; ++i) {
+  for (int i = 0; i < LDA; ++i) {
     const int r = 32 * i + r0;
     const int64_t gv = v0 + r < V ? r : V - 1 - v0;
-    const int64_t gm = m0 + r < M ? r : M - 1 - m0;
     a_off[i] = static_cast<uint32_t>(gv * d * 2 + c * 16);
+  }
+#pragma unroll
+  for (int i = 0; i < LDB; ++i) {
+    const int r = 32 * i + r0;
+    const int64_t gm = m0 + r < M ? r : M - 1 - m0;
     b_off[i] = static_cast<uint32_t>(gm * d * 2 + c * 16);
   }
-  u32x4 ra[2][LD], rb[2][LD];
+  u32x4 ra[2][LDA], rb[2][LDB];
 
   f32x16 acc[NRB][NCB];
 #pragma unroll
@@ -889,33 +910,32 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
   };
   const int nk = d / BK;
   // global -> registers (stage s, clamped to the last stage) and registers -> LDS, one 16-byte
-  // load of one operand at a time (q < LD: w, else h)
+  // load of one operand at a time (q < LDA: w, else h)
   auto gload = [&](auto buf_c, int s, int q) {
     constexpr int buf = decltype(buf_c)::value;
     const int koff = min(s, nk - 1) * ROWB;
-    if (q < LD)
+    if (q < LDA)
       ra[buf][q] = *reinterpret_cast<const u32x4*>(a_tile + a_off[q] + koff);
     else
-      rb[buf][q - LD] = *reinterpret_cast<const u32x4*>(b_tile + b_off[q - LD] + koff);
+      rb[buf][q - LDA] = *reinterpret_cast<const u32x4*>(b_tile + b_off[q - LDA] + koff);
   };
   auto swrite = [&](auto buf_c, auto slot_c, int q) {
     constexpr int buf = decltype(buf_c)::value, slot = decltype(slot_c)::value;
-    if (q < LD)
+    if (q < LDA)
       *reinterpret_cast<u32x4*>(sA[slot] + lds0 + q * 32 * ROWB) = ra[buf][q];
     else
-      *reinterpret_cast<u32x4*>(sB[slot] + lds0 + (q - LD) * 32 * ROWB) = rb[buf][q - LD];
+      *reinterpret_cast<u32x4*>(sB[slot] + lds0 + (q - LDA) * 32 * ROWB) = rb[buf][q - LDA];
   };
-  constexpr int NF = NRB + NCB, NQ = NRB * NCB, NSLOT = NQ / 2;
   auto frag_of = [](int f) { return f == 0 ? 0 : (f <= NCB ? NRB + f - 1 : f - NCB); };
 
   // Prologue: stage 0 in LDS slot 0, stage 1 in registers (buffer 1), stage 2 in flight
   // (buffer 0), stage 0's first fragments loaded.
 #pragma unroll
-  for (int q = 0; q < 2 * LD; ++q) gload(std::integral_constant<int, 0>{}, 0, q);
+  for (int q = 0; q < NLD; ++q) gload(std::integral_constant<int, 0>{}, 0, q);
 #pragma unroll
-  for (int q = 0; q < 2 * LD; ++q) gload(std::integral_constant<int, 1>{}, 1, q);
+  for (int q = 0; q < NLD; ++q) gload(std::integral_constant<int, 1>{}, 1, q);
 #pragma unroll
-  for (int q = 0; q < 2 * LD; ++q) {
+  for (int q = 0; q < NLD; ++q) {
     swrite(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, q);
     gload(std::integral_constant<int, 0>{}, 2, q);
   }
@@ -944,25 +964,29 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
       for (int i = 0; i < NSLOT; ++i) {
         mfma(cur, 2 * i);
         mfma(cur, 2 * i + 1);
-        if (st < KS - 1) {
-          load_frag(cur ^ 1, sA[j], sB[j], st + 1, frag_of(i));
-        } else {
-          load_frag(0, sA[jn], sB[jn], 0, frag_of(i));
+        // Fragments i NF / NSLOT .. (i + 1) NF / NSLOT - 1 of the next k step (in the order
+        // the MFMAs consume them).
+#pragma unroll
+        for (int f = i * NF / NSLOT; f < (i + 1) * NF / NSLOT; ++f) {
+          if (st < KS - 1)
+            load_frag(cur ^ 1, sA[j], sB[j], st + 1, frag_of(f));
+          else
+            load_frag(0, sA[jn], sB[jn], 0, frag_of(f));
         }
         {
-          // Register q is written to LDS at slot q TS / 2LD of the first kSpread k steps and
+          // Register q is written to LDS at slot q TS / NLD of the first kSpread k steps and
           // reloaded kShift slots later.
           constexpr int TS = kSpread * NSLOT;
           const int g = st * NSLOT + i;
           if (st < kSpread) {
 #pragma unroll
-            for (int q = g * 2 * LD / TS; q < (g + 1) * 2 * LD / TS; ++q)
+            for (int q = g * NLD / TS; q < (g + 1) * NLD / TS; ++q)
               swrite(std::integral_constant<int, jn>{}, std::integral_constant<int, jn>{}, q);
           }
           const int gl = g - kShift;
           if (gl >= 0 && gl < TS) {
 #pragma unroll
-            for (int q = gl * 2 * LD / TS; q < (gl + 1) * 2 * LD / TS; ++q)
+            for (int q = gl * NLD / TS; q < (gl + 1) * NLD / TS; ++q)
               gload(std::integral_constant<int, jn>{}, kt + 3, q);
           }
         }
@@ -970,7 +994,6 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
       }
     }
   };
-  static_assert(NF == NSLOT, "one fragment load per MFMA pair");
   int kt0 = 0;
   for (; kt0 + 2 <= nk; kt0 += 2) {
     body(std::integral_constant<int, 0>{}, kt0);
@@ -986,19 +1009,22 @@ __global__ __launch_bounds__(rs::kThreads, 1) void head_bf16_rs_kernel(
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) asm volatile("" : "+a"(acc[rb_][cb]));
 
-  // The last stage's slot is free once every wave has passed that stage's barrier (its reads
-  // came before it; the last k step reads the other slot): 16 KB of it per wave for the stores.
-  const int jl = (nk - 1) & 1;
-  char* const xp = (jl ? (wave < 2 ? sA1 : sB1) : (wave < 2 ? sA0 : sB0)) + (wave & 1) * (TILE / 2);
-  static_assert(TILE / 2 >= 32 * 512, "16 KB of LDS per wave for the transposed stores");
   const int64_t v0w = v0 + wv * kVTile;
   if (v0w >= V) return;
-  if constexpr (EPI == kEpiExpand)
+  if constexpr (EPI == kEpiExpand) {
     expand_store<NRB, NCB>(acc, ea, M, V, v0w, m0 + wm * TM, lane);
-  else if constexpr (DBL_HEAD_XP)
+  } else if constexpr (DBL_HEAD_XP) {
+    // The last stage's slot is free once every wave has passed that stage's barrier (its reads
+    // came before it; the last k step reads the other slot): 16 KB of it per wave for the
+    // stores.
+    static_assert(C::NW == 4 && C::TILEA / 2 >= 32 * 512 && C::TILEB / 2 >= 32 * 512,
+                  "16 KB of LDS per wave for the transposed stores");
+    const int jl = (nk - 1) & 1;
+    char* const xp = (jl ? (wave < 2 ? sA1 : sB1) : (wave < 2 ? sA0 : sB0)) +
+                     (wave & 1) * (wave < 2 ? C::TILEA / 2 : C::TILEB / 2);
     tile_logsoftmax_store_lds<NRB, NCB, EPI == kEpiLogSoftmaxArgmax>(
         acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w, m0 + wm * TM, lane, ea.vec4, xp);
-  else
+  } else
     tile_logsoftmax_store<NRB, NCB, EPI == kEpiLogSoftmaxArgmax>(
         acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w, m0 + wm * TM, lane, ea.vec4);
 }
@@ -1142,11 +1168,11 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
 #ifndef DBL_HEAD_RS
 #define DBL_HEAD_RS 1
 #endif
-    if (DBL_HEAD_RS && a.d % rs::BK == 0) {
-      const int dm = static_cast<int>((a.M + rs::BM - 1) / rs::BM);
-      const int64_t dwg = ((a.V + rs::BV - 1) / rs::BV) * dm;
+    if (DBL_HEAD_RS && a.d % RsHead::BK == 0) {
+      const int dm = static_cast<int>((a.M + RsHead::BM - 1) / RsHead::BM);
+      const int64_t dwg = ((a.V + RsHead::BV - 1) / RsHead::BV) * dm;
       if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
-      const dim3 grid(static_cast<unsigned>(dwg)), block(rs::kThreads);
+      const dim3 grid(static_cast<unsigned>(dwg)), block(RsHead::kThreads);
       EpiArgs ea{};
       ea.tls = a.tls;
       ea.lmass = a.lmass;
@@ -1154,10 +1180,10 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
       ea.nT = nT;
       ea.vec4 = vec4;
       if (amax)
-        hipLaunchKernelGGL((head_bf16_rs_kernel<kEpiLogSoftmaxArgmax>), grid, block, 0, stream, h,
+        hipLaunchKernelGGL((head_bf16_rs_kernel<RsHead, kEpiLogSoftmaxArgmax>), grid, block, 0, stream, h,
                            w, ea, a.M, a.V, a.d, dm);
       else
-        hipLaunchKernelGGL((head_bf16_rs_kernel<kEpiLogSoftmax>), grid, block, 0, stream, h, w,
+        hipLaunchKernelGGL((head_bf16_rs_kernel<RsHead, kEpiLogSoftmax>), grid, block, 0, stream, h, w,
                            ea, a.M, a.V, a.d, dm);
     } else if (a.d % DCfg::BK == 0) {
       const int dm = static_cast<int>((a.M + DCfg::BM - 1) / DCfg::BM);
@@ -1248,10 +1274,30 @@ hipError_t launch_expand_cfg(const ExpandArgs& a, int64_t N, hipStream_t stream)
   return hipGetLastError();
 }
 
+// Register-staged expander for few trunk rows: 128 output features x 256 rows per workgroup, so
+// every weight row is streamed once and the grid still covers the chip.
+template <class C>
+hipError_t launch_expand_rs(const ExpandArgs& a, int64_t N, hipStream_t stream) {
+  const int dm = static_cast<int>((a.M + C::BM - 1) / C::BM);
+  const int64_t dwg = ((N + C::BV - 1) / C::BV) * dm;
+  if (dwg > 0x7fffffff || a.d % C::BK != 0) return hipErrorInvalidConfiguration;
+  EpiArgs ea{};
+  ea.out = static_cast<__bf16*>(a.out);
+  ea.bias = static_cast<const __bf16*>(a.c);
+  ea.hres = static_cast<const __bf16*>(a.h);
+  ea.dres = a.d;
+  hipLaunchKernelGGL((head_bf16_rs_kernel<C, kEpiExpand>), dim3(static_cast<unsigned>(dwg)),
+                     dim3(C::kThreads), 0, stream, static_cast<const __bf16*>(a.h),
+                     static_cast<const __bf16*>(a.W), ea, a.M, N, a.d, dm);
+  return hipGetLastError();
+}
 hipError_t launch_expand(const ExpandArgs& a, hipStream_t stream) {
   const int64_t N = a.R * a.d;
   const int64_t wg256 = ((N + DCfg::BV - 1) / DCfg::BV) * ((a.M + DCfg::BM - 1) / DCfg::BM);
-  if (wg256 < kCus) return launch_expand_cfg<ECfg>(a, N, stream);
+  if (wg256 < kCus) {
+    if (a.d % RsNarrow::BK == 0) return launch_expand_rs<RsNarrow>(a, N, stream);
+    return launch_expand_cfg<ECfg>(a, N, stream);
+  }
   return launch_expand_cfg<DCfg>(a, N, stream);
 }
 
