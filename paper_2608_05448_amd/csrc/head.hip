@@ -6,9 +6,9 @@
 // 16 logits of one branch row. The per-tile (128 ids) max and sum of exponentials therefore
 // reduce in registers plus one cross-half exchange, and the tile-normalised log-probs are
 // stored straight from the accumulators: logits never reach memory. Operand feeds, by hidden
-// size: d % 64 == 0, 64-deep stages staged through registers (the main path); d % 32 == 0,
-// 32-deep stages copied global -> LDS directly (also used by the branch expander); otherwise a
-// register-staged kernel with padded LDS rows.
+// size: d % 64 == 0, 64-deep stages staged through registers (the main path; the branch
+// expander uses the same kernel with narrower tiles); d % 32 == 0, 32-deep stages copied global
+// -> LDS directly; otherwise a register-staged kernel with padded LDS rows.
 //
 // fp32 path: a plain fp32 kernel for fp32 inputs (small problems).
 #include <hip/hip_runtime.h>
