@@ -665,6 +665,9 @@ __device__ void filter_general(const FilterArgs& a, const float* in, float* out,
 // the row. Returns false (nothing written) if the cut's bin holds more than kCandCap tokens.
 constexpr int kNucBins = 2048;
 constexpr float kNucScale = kNucBins / 27.8f;  // P(v) = 0 below s - m = -40 ln 2 = -27.73
+// Every token of a bin <= kNucSureBin has s - m > -27.16, so detexp32 > 1.5e-12 > 2^-40 and
+// P(v) >= 1: when the cut's bin is one of them, the later passes need only the bins.
+constexpr int kNucSureBin = 2000;
 
 __device__ bool filter_nucleus(const FilterArgs& a, const float* in, float* out, bool vec,
                                uint64_t* bins, uint64_t* cand, uint64_t* red, int* sh_n) {
@@ -678,6 +681,13 @@ __device__ bool filter_nucleus(const FilterArgs& a, const float* in, float* out,
     mk = x > mk ? x : mk;
   });
   const float m = __fdiv_rn(key_value(static_cast<uint32_t>(block_max_u64(mk, red))), T);
+  // s = fl32(x / T); x / 1 is x exactly, so T = 1 needs no division
+  auto scan = [&](auto fn) {
+    if (T == 1.0f)
+      row_scan_raw<2>(in, V, vec, fn);
+    else
+      row_scan<2>(in, V, T, vec, fn);
+  };
   auto mass_bin = [&](float sv, uint64_t* P) {
     const float d = __fsub_rn(sv, m);
     *P = quant40(detexp32(d));
@@ -686,7 +696,7 @@ __device__ bool filter_nucleus(const FilterArgs& a, const float* in, float* out,
   // 2. integer mass per bin
   for (int i = tid; i < kNucBins; i += kFT) bins[i] = 0;
   __syncthreads();
-  row_scan<2>(in, V, T, vec, [&](int64_t, float sv) {
+  scan([&](int64_t, float sv) {
     uint64_t P;
     const int b = mass_bin(sv, &P);
     if (P) atomicAdd(reinterpret_cast<unsigned long long*>(&bins[b]), static_cast<unsigned long long>(P));
@@ -722,14 +732,27 @@ __device__ bool filter_nucleus(const FilterArgs& a, const float* in, float* out,
   const int bstar = static_cast<int>(red[0]);
   const uint64_t before = red[1];
   __syncthreads();
+  auto bin_of = [&](float sv) {
+    return min(kNucBins - 1, static_cast<int>(__fmul_rn(-__fsub_rn(sv, m), kNucScale)));
+  };
+  const bool sure = bstar <= kNucSureBin;
   // 3. the crossing bin's tokens, then their order
-  row_scan<2>(in, V, T, vec, [&](int64_t v, float sv) {
-    uint64_t P;
-    if (mass_bin(sv, &P) == bstar && P) {
-      const int slot = atomicAdd(sh_n, 1);
-      if (slot < kCandCap) cand[slot] = visit_key(order_key(sv), v);
-    }
-  });
+  if (sure) {
+    scan([&](int64_t v, float sv) {
+      if (bin_of(sv) == bstar) {
+        const int slot = atomicAdd(sh_n, 1);
+        if (slot < kCandCap) cand[slot] = visit_key(order_key(sv), v);
+      }
+    });
+  } else {
+    scan([&](int64_t v, float sv) {
+      uint64_t P;
+      if (mass_bin(sv, &P) == bstar && P) {
+        const int slot = atomicAdd(sh_n, 1);
+        if (slot < kCandCap) cand[slot] = visit_key(order_key(sv), v);
+      }
+    });
+  }
   __syncthreads();
   const int n = *sh_n;
   __syncthreads();
@@ -765,13 +788,22 @@ __device__ bool filter_nucleus(const FilterArgs& a, const float* in, float* out,
   const uint64_t cut = cand[nkeep - 1];
   const double lse = log(static_cast<double>(kmass)) - 40.0 * 0.6931471805599453;
   // 4. output row
-  row_scan<2>(in, V, T, vec, [&](int64_t v, float sv) {
-    uint64_t P;
-    const int b = mass_bin(sv, &P);
-    const bool kept = P && (b < bstar || (b == bstar && visit_key(order_key(sv), v) >= cut));
-    out[v] = kept ? static_cast<float>(static_cast<double>(sv) - static_cast<double>(m) - lse)
-                  : -INFINITY;
-  });
+  if (sure) {
+    scan([&](int64_t v, float sv) {
+      const int b = bin_of(sv);
+      const bool kept = b < bstar || (b == bstar && visit_key(order_key(sv), v) >= cut);
+      out[v] = kept ? static_cast<float>(static_cast<double>(sv) - static_cast<double>(m) - lse)
+                    : -INFINITY;
+    });
+  } else {
+    scan([&](int64_t v, float sv) {
+      uint64_t P;
+      const int b = mass_bin(sv, &P);
+      const bool kept = P && (b < bstar || (b == bstar && visit_key(order_key(sv), v) >= cut));
+      out[v] = kept ? static_cast<float>(static_cast<double>(sv) - static_cast<double>(m) - lse)
+                    : -INFINITY;
+    });
+  }
   return true;
 }
 
