@@ -27,6 +27,11 @@ def _logits(N, V, seed, ties=False):
         for r in range(N):
             top = np.argsort(-g[r])[:40]
             g[r, top] = np.float32(7.0) + np.arange(40, dtype=np.float32) * np.spacing(np.float32(7.0))
+    elif ties == "tail":   # one token at 0, the rest ~27.5 below it, where the integer masses
+        # are 0, 1 or 2: a nucleus with p near 1 cuts there, in a bin past 2000 (the kernel then
+        # computes the masses in every pass, not the bins alone)
+        g = (-27.5 + 0.15 * synth.make_uniform_logits((N, V), seed).numpy()).astype(np.float32)
+        g[:, 0] = 0.0
     elif ties:   # coarse values: many equal logits at both cuts
         g = np.round(g * 2.0) / 2.0
     return g.astype(np.float32)
@@ -64,6 +69,7 @@ CASES = [
     ("nucleus-top-k-ge-V", 2, 3000, 1.0, 5000, 0.8, False),
     ("nucleus-ragged-vocab", 3, 50001, 0.7, 0, 0.8, False),
     ("flat-row-nucleus", 2, 151936, 1.0, 0, 0.95, "flat"),
+    ("nucleus-cut-in-the-tail", 2, 151936, 1.0, 0, 0.9999999, "tail"),
 ]
 
 
