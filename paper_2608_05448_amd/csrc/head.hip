@@ -911,13 +911,16 @@ __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_rs_kernel(
   const int nk = d / BK;
   // global -> registers (stage s, clamped to the last stage) and registers -> LDS, one 16-byte
   // load of one operand at a time (q < LDA: w, else h)
+  // Stages past the last (the pipeline's final three reloads) read the tile's first 16 bytes in
+  // every lane: one cached request instead of a stage of operand traffic; never consumed.
   auto gload = [&](auto buf_c, int s, int q) {
     constexpr int buf = decltype(buf_c)::value;
-    const int koff = min(s, nk - 1) * ROWB;
+    const bool live = s < nk;
     if (q < LDA)
-      ra[buf][q] = *reinterpret_cast<const u32x4*>(a_tile + a_off[q] + koff);
+      ra[buf][q] = *reinterpret_cast<const u32x4*>(a_tile + (live ? a_off[q] + s * ROWB : 0u));
     else
-      rb[buf][q - LDA] = *reinterpret_cast<const u32x4*>(b_tile + b_off[q - LDA] + koff);
+      rb[buf][q - LDA] =
+          *reinterpret_cast<const u32x4*>(b_tile + (live ? b_off[q - LDA] + s * ROWB : 0u));
   };
   auto swrite = [&](auto buf_c, auto slot_c, int q) {
     constexpr int buf = decltype(buf_c)::value, slot = decltype(slot_c)::value;
