@@ -36,6 +36,11 @@ __global__ __launch_bounds__(64) void greedy_sample_kernel(GreedyArgs a) {
     a.x_out[b * k_.K + k] = z >= 0 ? a.xhat[(b * k_.K + k) * k_.R + z] : -1;
 }
 
+// Positions per block whose inputs the chain stages in LDS before walking them (drafted token,
+// branch tokens and the target log-probabilities at both): the walk then waits on no memory.
+constexpr int kGreedyStageK = 64;
+constexpr int kGreedyStageKR = 1024;
+
 __global__ __launch_bounds__(64) void greedy_chain_kernel(GreedyArgs a) {
   const BlockArgs& k_ = a.blk;
   const int64_t b = blockIdx.x;
@@ -45,6 +50,26 @@ __global__ __launch_bounds__(64) void greedy_chain_kernel(GreedyArgs a) {
   const uint64_t seq = static_cast<uint64_t>(k_.seq_offset + b);
   __shared__ int32_t s_tok[64];
   __shared__ double s_w[64];
+  __shared__ int32_t s_x[kGreedyStageK];
+  __shared__ float s_px[kGreedyStageK];
+  __shared__ int32_t s_t[kGreedyStageKR];
+  __shared__ float s_pt[kGreedyStageKR];
+  const bool staged = k_.K <= kGreedyStageK && k_.K * k_.R <= kGreedyStageKR;
+  if (staged) {  // every gather of the walk, issued together
+    const int K = static_cast<int>(k_.K), KR = K * R;
+    for (int k = lane; k < K; k += 64) s_x[k] = a.x[b * k_.K + k];
+    for (int i = lane; i < KR; i += 64) s_t[i] = a.xhat[b * k_.K * k_.R + i];
+    __syncthreads();
+    for (int k = lane; k < K; k += 64) {
+      const int32_t xk = s_x[k];
+      s_px[k] = in_vocab(xk, V) ? a.logp[(b * a.Kp + k) * V + xk] : 0.0f;
+    }
+    for (int i = lane; i < KR; i += 64) {
+      const int32_t t = s_t[i];
+      s_pt[i] = in_vocab(t, V) ? a.logp[(b * a.Kp + i / R) * V + t] : 0.0f;
+    }
+    __syncthreads();
+  }
   const double L0 = prior_log_weight(k_.prior + b * k_.R, R, k_.z_temp);
   const bool want_beta = a.beta || a.exp_len;
   bool consistent = lane < R;
@@ -55,14 +80,15 @@ __global__ __launch_bounds__(64) void greedy_chain_kernel(GreedyArgs a) {
     const int64_t row = (b * k_.K + k) * k_.R;
     const double w = normalize_weight(consistent ? L0 : -INFINITY, R);
     if (lane < R) a.wpost[row + lane] = w;
-    const int32_t xk = a.x[b * k_.K + k];
-    const int32_t t = lane < R ? a.xhat[row + lane] : -1;
+    const int32_t xk = staged ? s_x[k] : a.x[b * k_.K + k];
+    const int32_t t = lane < R ? (staged ? s_t[k * R + lane] : a.xhat[row + lane]) : -1;
     const bool match = lane < R && t == xk;
     const float* prow = a.logp + (b * a.Kp + k) * V;
     if (!a.trajectory) {
       double Q = 0.0;
-      for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, __shfl(match ? w : 0.0, z));
-      const double P = in_vocab(xk, V) ? static_cast<double>(detexp32(prow[xk])) : 0.0;
+      for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, lane_f64(match ? w : 0.0, z));
+      const float px = staged ? s_px[k] : (in_vocab(xk, V) ? prow[xk] : 0.0f);
+      const double P = in_vocab(xk, V) ? static_cast<double>(detexp32(px)) : 0.0;
       const double A = Q > 0.0 ? fmin(1.0, P / Q) : (P > 0.0 ? 1.0 : 0.0);
       prodA = __dmul_rn(prodA, A);
       al = __dadd_rn(al, prodA);
@@ -90,7 +116,8 @@ __global__ __launch_bounds__(64) void greedy_chain_kernel(GreedyArgs a) {
             q = __dadd_rn(q, s_w[z]);
           }
         }
-        if (first) contrib = fmin(exp(static_cast<double>(prow[t])), q);
+        const float pt = staged ? s_pt[k * R + lane] : prow[t];
+        if (first) contrib = fmin(exp(static_cast<double>(pt)), q);
       }
       const double beta_k = wave_sum_f64(contrib);
       if (a.beta && lane == 0) a.beta[b * k_.K + k] = static_cast<float>(beta_k);
