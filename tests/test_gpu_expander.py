@@ -29,6 +29,7 @@ EXPAND_CASES = [
     ("qwen3-4b-paper-R", 1, 16, 4, 2560),
     ("qwen3-8b-R8", 16, 16, 8, 4096),
     ("max-categories", 1, 3, 64, 64),
+    ("two-row-tiles-ragged", 2, 150, 2, 128),   # 300 trunk rows: a second, partial 256-row tile
 ]
 
 
