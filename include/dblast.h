@@ -57,8 +57,10 @@
  * Conventions for every call:
  *  - Ownership: every data pointer is a device pointer owned by the caller; the library never
  *    allocates device memory. Scratch space is a caller-provided device workspace of at least
- *    dbl_workspace_bytes(op, shape) bytes, 256-byte aligned. Array arguments must be 16-byte
- *    aligned (vector loads and stores; any allocator's base pointer is).
+ *    dbl_workspace_bytes(op, shape) bytes, 256-byte aligned. Every array argument must be
+ *    16-byte aligned (the kernels use 16-byte vector loads and stores; any allocator's base
+ *    pointer is, a view starting at an element offset may not be); a misaligned one is
+ *    DBL_EINVAL.
  *  - Streams: work is enqueued on `stream` (a hipStream_t; NULL is the default stream) and the
  *    call returns without waiting. Outputs are valid once the stream reaches that point. No
  *    call allocates, frees, copies, sets memory or synchronises: workspaces are cleared by
@@ -66,8 +68,8 @@
  *  - Errors: a non-zero dbl_status is returned before anything is launched when an argument is
  *    invalid; DBL_EHIP reports a failed launch. dbl_last_error() gives a message for the
  *    calling thread's last failure. Data-dependent problems (NaN inputs) are not detected.
- *  - Shapes: K, R, d, V >= 1, B >= 0 (B = 0 is a no-op), R <= 64, V < 2^24, d % 8 == 0 for the
- *    head, M * V < 2^62.
+ *  - Shapes: K, R, d, V >= 1, B >= 0 (B = 0 is a no-op), R <= 64, V < 2^24, d <= 2^20 and
+ *    d % 8 == 0 for the bf16 head, M * V < 2^62.
  *  - Thread safety: calls hold no global mutable state apart from the per-thread error text;
  *    concurrent calls on different streams with disjoint outputs and workspaces are safe.
  */
@@ -85,7 +87,7 @@ extern "C" {
 
 typedef enum {
   DBL_OK = 0,
-  DBL_EINVAL = 1,      /* null pointer, negative temperature, bad Kp, unknown op/dtype */
+  DBL_EINVAL = 1,      /* null or misaligned array, negative temperature, bad Kp, ... */
   DBL_ESHAPE = 2,      /* a dimension outside the supported range */
   DBL_EDTYPE = 3,      /* unsupported element type */
   DBL_EWORKSPACE = 4,  /* workspace missing, too small or misaligned */
@@ -141,8 +143,9 @@ const char* dbl_last_error(void);
  *          the same fp32 logits, so tls, lmass and lse are identical with or without it
  *   ws     workspace of dbl_workspace_bytes(DBL_OP_HEAD, shape) bytes (M * 8); needed only
  *          when argmax is requested, otherwise may be 0 and NULL
- * Errors: DBL_EINVAL for null pointers, DBL_EDTYPE for other dt, DBL_ESHAPE when d % 8 != 0
- * or a dimension is out of range, DBL_EWORKSPACE when argmax is requested without workspace.
+ * Errors: DBL_EINVAL for null or misaligned pointers, DBL_EDTYPE for other dt, DBL_ESHAPE when
+ * d % 8 != 0 (bf16), d > 2^20 or a dimension is out of range, DBL_EWORKSPACE when argmax is
+ * requested without workspace.
  */
 dbl_status dbl_head_logprobs(dbl_shape shape, int dt, const void* h, const void* w, float* tls,
                              float* lmass, float* lse, int32_t* argmax, void* ws,

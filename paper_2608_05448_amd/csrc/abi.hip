@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <cstdio>
+#include <initializer_list>
 #include <string>
 
 #include "../../include/dblast.h"
@@ -33,10 +34,20 @@ dbl_status check_shape(const dbl_shape& s, bool need_d) {
   if (s.R > dbl::kMaxR) return fail(DBL_ESHAPE, "R must be <= 64");
   if (s.V >= (int64_t(1) << 24)) return fail(DBL_ESHAPE, "V must be < 2^24");
   if (s.K > (int64_t(1) << 20)) return fail(DBL_ESHAPE, "K must be <= 2^20");
-  if (need_d && (s.d < 1 || s.d > (int64_t(1) << 30)))
-    return fail(DBL_ESHAPE, "d must be in [1, 2^30]");
+  // The bf16 head kernels address a tile's operand rows with 32-bit byte offsets (up to 512 d).
+  if (need_d && (s.d < 1 || s.d > (int64_t(1) << 20)))
+    return fail(DBL_ESHAPE, "d must be in [1, 2^20]");
   const double rows = static_cast<double>(s.B) * s.K * s.R;
   if (rows * static_cast<double>(s.V) >= 4.0e18) return fail(DBL_ESHAPE, "B*K*R*V too large");
+  return ok();
+}
+
+// Every array is read and written with 16-byte vector accesses, so each must be 16-byte
+// aligned. NULL (an optional array that is not passed) is not checked here.
+dbl_status check_aligned(std::initializer_list<std::pair<const void*, const char*>> arrays) {
+  for (const auto& a : arrays)
+    if (reinterpret_cast<uintptr_t>(a.first) % 16 != 0)
+      return fail(DBL_EINVAL, std::string(a.second) + " is not 16-byte aligned");
   return ok();
 }
 
@@ -148,7 +159,7 @@ dbl_status check_block_inputs(const dbl_shape& s, const float* tls, const float*
   if (!tls || !lmass || !lse || !prior) return fail(DBL_EINVAL, "NULL input pointer");
   if (!(z_temp >= 0.0f) || isinf(z_temp))
     return fail(DBL_EINVAL, "z_temp must be finite and >= 0");
-  return ok();
+  return check_aligned({{tls, "tls"}, {lmass, "lmass"}, {lse, "lse"}, {prior, "prior_logits"}});
 }
 
 dbl_status check_greedy_inputs(const dbl_shape& s, const int32_t* xhat, const float* prior,
@@ -157,7 +168,7 @@ dbl_status check_greedy_inputs(const dbl_shape& s, const int32_t* xhat, const fl
   if (!xhat || !prior) return fail(DBL_EINVAL, "NULL input pointer");
   if (!(z_temp >= 0.0f) || isinf(z_temp))
     return fail(DBL_EINVAL, "z_temp must be finite and >= 0");
-  return ok();
+  return check_aligned({{xhat, "x_hat"}, {prior, "prior_logits"}});
 }
 
 dbl::GreedyArgs greedy_args(const dbl_shape& s, const int32_t* xhat, const float* prior,
@@ -202,6 +213,9 @@ dbl_status dbl_head_logprobs(dbl_shape s, int dt, const void* h, const void* w, 
   if (dt != DBL_F32 && dt != DBL_BF16) return fail(DBL_EDTYPE, "dtype must be DBL_F32 or DBL_BF16");
   if (dt == DBL_BF16 && s.d % 8 != 0) return fail(DBL_ESHAPE, "bf16 head needs d % 8 == 0");
   if (!h || !w || !tls || !lmass || !lse) return fail(DBL_EINVAL, "NULL pointer");
+  if (dbl_status st = check_aligned({{h, "h"}, {w, "w"}, {tls, "tls"}, {lmass, "lmass"},
+                                     {lse, "lse"}, {argmax, "argmax"}}))
+    return st;
   WsLayout L;
   if (argmax) {
     if (dbl_status st = check_ws(DBL_OP_HEAD, s, ws, ws_bytes, &L)) return st;
@@ -228,6 +242,7 @@ dbl_status dbl_sample_block(dbl_shape s, const float* tls, const float* lmass,
                             int32_t* x_out, void* ws, size_t ws_bytes, void* stream) {
   if (dbl_status st = check_block_inputs(s, tls, lmass, lse, prior_logits, z_temp)) return st;
   if (!z_out || !x_out) return fail(DBL_EINVAL, "NULL output pointer");
+  if (dbl_status st = check_aligned({{z_out, "z_out"}, {x_out, "x_out"}})) return st;
   WsLayout L;
   if (dbl_status st = check_ws(DBL_OP_SAMPLE, s, ws, ws_bytes, &L)) return st;
   if (s.B == 0) return ok();
@@ -249,6 +264,10 @@ dbl_status dbl_verify_block(dbl_shape s, const float* tls, const float* lmass,
   if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
   if (!n_accept || !next_token) return fail(DBL_EINVAL, "NULL output pointer");
   if (Kp != s.K && Kp != s.K + 1) return fail(DBL_EINVAL, "Kp must be K or K + 1");
+  if (dbl_status st = check_aligned({{x, "x"}, {logp, "logp"}, {n_accept, "n_accept"},
+                                     {next_token, "next_token"}, {accept_mass, "accept_mass"},
+                                     {al_expected, "al_expected"}, {exp_len, "exp_len"}}))
+    return st;
   WsLayout L;
   if (dbl_status st = check_ws(DBL_OP_VERIFY, s, ws, ws_bytes, &L)) return st;
   if (s.B == 0) return ok();
@@ -278,6 +297,9 @@ dbl_status dbl_expected_len(dbl_shape s, const float* tls, const float* lmass,
   if (dbl_status st = check_block_inputs(s, tls, lmass, lse, prior_logits, z_temp)) return st;
   if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
   if (!exp_len) return fail(DBL_EINVAL, "NULL output pointer");
+  if (dbl_status st = check_aligned({{x, "x"}, {logp, "logp"}, {beta, "beta"},
+                                     {exp_len, "exp_len"}}))
+    return st;
   WsLayout L;
   if (dbl_status st = check_ws(DBL_OP_EXPECTED_LEN, s, ws, ws_bytes, &L)) return st;
   if (s.B == 0) return ok();
@@ -306,6 +328,7 @@ dbl_status dbl_sample_greedy(dbl_shape s, const int32_t* x_hat, const float* pri
                              int32_t* z_out, int32_t* x_out, void* stream) {
   if (dbl_status st = check_greedy_inputs(s, x_hat, prior_logits, z_temp)) return st;
   if (!z_out || !x_out) return fail(DBL_EINVAL, "NULL output pointer");
+  if (dbl_status st = check_aligned({{z_out, "z_out"}, {x_out, "x_out"}})) return st;
   if (s.B == 0) return ok();
   dbl::GreedyArgs a = greedy_args(s, x_hat, prior_logits, z_temp, seed, step, seq_offset);
   a.z_out = z_out;
@@ -323,6 +346,10 @@ dbl_status dbl_verify_greedy(dbl_shape s, const int32_t* x_hat, const float* pri
   if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
   if (!n_accept || !next_token) return fail(DBL_EINVAL, "NULL output pointer");
   if (Kp != s.K && Kp != s.K + 1) return fail(DBL_EINVAL, "Kp must be K or K + 1");
+  if (dbl_status st = check_aligned({{x, "x"}, {logp, "logp"}, {n_accept, "n_accept"},
+                                     {next_token, "next_token"}, {accept_mass, "accept_mass"},
+                                     {al_expected, "al_expected"}, {exp_len, "exp_len"}}))
+    return st;
   WsLayout L;
   if (dbl_status st = check_ws(DBL_OP_VERIFY_GREEDY, s, ws, ws_bytes, &L)) return st;
   if (s.B == 0) return ok();
@@ -351,6 +378,9 @@ dbl_status dbl_expected_len_greedy(dbl_shape s, const int32_t* x_hat,
   if (dbl_status st = check_greedy_inputs(s, x_hat, prior_logits, z_temp)) return st;
   if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
   if (!exp_len) return fail(DBL_EINVAL, "NULL output pointer");
+  if (dbl_status st = check_aligned({{x, "x"}, {logp, "logp"}, {beta, "beta"},
+                                     {exp_len, "exp_len"}}))
+    return st;
   WsLayout L;
   if (dbl_status st = check_ws(DBL_OP_EXPECTED_LEN_GREEDY, s, ws, ws_bytes, &L)) return st;
   if (s.B == 0) return ok();
@@ -375,6 +405,9 @@ dbl_status dbl_acceptance_objective(dbl_shape s, const float* tls, const float* 
   if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
   if (!ell_tau || !J || !nll) return fail(DBL_EINVAL, "NULL output pointer");
   if (!(tau > 0.0f) || isinf(tau)) return fail(DBL_EINVAL, "tau must be finite and > 0");
+  if (dbl_status st = check_aligned({{x, "x"}, {logp, "logp"}, {log_r, "log_r"}, {S, "S"},
+                                     {ell_tau, "ell_tau"}, {J, "J"}, {nll, "nll"}}))
+    return st;
   if (s.B == 0) return ok();
   dbl::ObjectiveArgs a{};
   a.blk = block_args(s, tls, lmass, lse, prior_logits, z_temp, 0, 0, 0);
@@ -399,6 +432,8 @@ dbl_status dbl_expand_branches(dbl_shape s, const void* h, const void* W, const 
   if (static_cast<double>(s.B) * s.K * s.R * s.d >= 4.0e18)
     return fail(DBL_ESHAPE, "B*K*R*d too large");
   if (!h || !W || !c || !h_out) return fail(DBL_EINVAL, "NULL pointer");
+  if (dbl_status st = check_aligned({{h, "h"}, {W, "W"}, {c, "c"}, {h_out, "h_out"}}))
+    return st;
   if (s.B == 0) return ok();
   dbl::ExpandArgs a;
   a.M = s.B * s.K;
@@ -416,6 +451,9 @@ dbl_status dbl_prior_head(dbl_shape s, const void* h_anchor, const void* U, cons
   if (s.B < 0 || s.R < 1 || s.R > dbl::kMaxR || s.d < 1 || s.d > (int64_t(1) << 30))
     return fail(DBL_ESHAPE, "need B >= 0, 1 <= R <= 64 and 1 <= d <= 2^30");
   if (!h_anchor || !U || !e || !prior_logits) return fail(DBL_EINVAL, "NULL pointer");
+  if (dbl_status st = check_aligned({{h_anchor, "h_anchor"}, {U, "U"}, {e, "e"},
+                                     {prior_logits, "prior_logits"}}))
+    return st;
   if (s.B == 0) return ok();
   dbl::PriorHeadArgs a;
   a.B = s.B;
@@ -436,6 +474,7 @@ dbl_status dbl_target_logprobs(int64_t N, int64_t V, const float* logits, float 
   if (static_cast<double>(N) * static_cast<double>(V) >= 4.0e18)
     return fail(DBL_ESHAPE, "N*V too large");
   if (!logits || !logp) return fail(DBL_EINVAL, "NULL pointer");
+  if (dbl_status st = check_aligned({{logits, "logits"}, {logp, "logp"}})) return st;
   {
     const uintptr_t a0 = reinterpret_cast<uintptr_t>(logits), b0 = reinterpret_cast<uintptr_t>(logp);
     const uintptr_t len = static_cast<uintptr_t>(N) * static_cast<uintptr_t>(V) * sizeof(float);
@@ -474,6 +513,8 @@ dbl_status dbl_early_determinism(int64_t M, int64_t b, int64_t V, const int32_t*
     return fail(DBL_ESHAPE, "need M >= 0, b >= 1, 1 <= V < 2^24");
   if (static_cast<double>(M) * b * V >= 4.0e18) return fail(DBL_ESHAPE, "M*b*V too large");
   if (!x || !logp || !terms) return fail(DBL_EINVAL, "NULL pointer");
+  if (dbl_status st = check_aligned({{x, "x"}, {logp, "logp"}, {terms, "terms"}, {mean, "mean"}}))
+    return st;
   if (M == 0) return ok();
   dbl::DeterminismArgs a;
   a.M = M;
@@ -493,7 +534,7 @@ dbl_status dbl_stream_read_probe(const void* buf, int64_t bytes, float* partials
   if (bytes < 0 || bytes % 16 != 0) return fail(DBL_ESHAPE, "bytes must be a multiple of 16");
   if (n_partials < 1 || n_partials > (int64_t(1) << 20))
     return fail(DBL_ESHAPE, "need 1 <= n_partials <= 2^20");
-  if (reinterpret_cast<uintptr_t>(buf) % 16 != 0) return fail(DBL_EINVAL, "buf not 16-byte aligned");
+  if (dbl_status st = check_aligned({{buf, "buf"}, {partials, "partials"}})) return st;
   return hip_status(dbl::launch_read_probe(buf, bytes, partials, n_partials,
                                            static_cast<hipStream_t>(stream)),
                     "read probe launch");
