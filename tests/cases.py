@@ -29,7 +29,7 @@ class BlockCase:
     """Branch log-probs (oracle head on synthetic h, w), category logits and a target."""
 
     def __init__(self, B, K, R, V, d=32, seed=0, target="aligned", kp_extra=1, T=1.0,
-                 q_sharp=2.0):
+                 q_sharp=2.0, noise=0.3):
         self.B, self.K, self.R, self.V, self.d = B, K, R, V, d
         h = synth.make_uniform_logits((B * K * R, d), seed * 7 + 1).to(torch.float32)
         w = synth.make_uniform_logits((V, d), seed * 7 + 2, scale=q_sharp / math.sqrt(d))
@@ -43,16 +43,35 @@ class BlockCase:
         self.ell = synth.make_uniform_logits((B, R), seed * 7 + 3).to(torch.float32).numpy()
         Kp = K + kp_extra
         g = synth.make_uniform_logits((B, Kp, V), seed * 7 + 4, scale=2.0)
-        if target == "aligned":
-            # The target at position k follows branch (b + k) % R of the drafter, plus noise:
-            # most drafted tokens then have comparable p and q and the accept path is exercised.
+        if target in ("aligned", "aligned-block"):
+            # "aligned": the target at position k follows branch (b + k) % R of the drafter,
+            # plus noise, so most drafted tokens have comparable p and q. "aligned-block": every
+            # position of block b follows branch b % R, so blocks whose drawn category is b % R
+            # are often accepted in full (and the bonus row is drawn from).
             base = torch.from_numpy(self.lq.astype(np.float64))
-            idx = (torch.arange(B)[:, None] + torch.arange(K)[None, :]) % R
+            shift = torch.arange(K)[None, :] if target == "aligned" else 0 * torch.arange(K)[None, :]
+            idx = (torch.arange(B)[:, None] + shift) % R
             follow = base[torch.arange(B)[:, None], torch.arange(K)[None, :], idx]
-            g[:, :K] = follow + 0.3 * g[:, :K]
+            g[:, :K] = follow + noise * g[:, :K]
         self.logp = synth.target_logprobs(g, T).numpy()
 
     def device(self):
         dev = "cuda"
         f = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
         return f(self.tls), f(self.lmass), f(self.lse), f(self.ell), f(self.logp)
+
+
+_ORACLE_FULL: dict = {}
+
+
+def oracle_full_head(name: str, h: torch.Tensor, w: torch.Tensor) -> np.ndarray:
+    """The oracle's branch log-probs [M, V] (binary32 flat form) for a whole workload's head,
+    from the exact inputs h [B, K, R, d] and w [V, d] the GPU consumed (binary64 GEMM and
+    log-softmax). Computed once per process for the most recent workload name."""
+    if name not in _ORACLE_FULL:
+        _ORACLE_FULL.clear()
+        d = h.shape[-1]
+        tls, lmass, lse = OH.head_factored(np32(h).reshape(-1, d), np32(w), v_chunk=8192)
+        _ORACLE_FULL[name] = OH.flat_logq(tls, lmass, lse)
+        del tls, lmass, lse
+    return _ORACLE_FULL[name]

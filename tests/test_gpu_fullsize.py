@@ -1,8 +1,10 @@
-"""Full-size GPU runs of the benchmark-scale workloads, checked on sampled outputs.
+"""Full-size GPU runs of the benchmark-scale workloads.
 
 Each test runs the whole hot path at the workload's real shape in the same launch
-configuration as the benchmark, then recomputes a few blocks end to end with the oracle
-(binary64 head on the same bf16 inputs, then the oracle's own draw and verification). Token
+configuration as the benchmark, then recomputes blocks end to end with the oracle (binary64
+head on the same bf16 inputs, then the oracle's own draw and verification): every block of the
+Qwen3-8B step at every target temperature, sampled blocks and steps of the objective and stress
+workloads. Token
 indices must agree exactly; any disagreement must be a certified near-tie (the GPU's fp32
 log-probs differ from the oracle's binary64 ones by ~1e-6, which can move a threshold across a
 boundary only when it lies within that margin). Real-valued outputs agree within 1e-4 relative.
@@ -45,7 +47,10 @@ def _near_tie_token(lq_row, r, got, want):
     return gap <= 1e-5 * Z
 
 
-def test_e2e_qwen3_8b_sampled_blocks_all_temperatures():
+def test_e2e_qwen3_8b_all_blocks_all_temperatures():
+    """The benchmark's step at the Qwen3-8B shape, every block: the oracle's binary64 head on the
+    same bf16 inputs, then its own draw and verification, at every target temperature."""
+    from cases import oracle_full_head
     from paper_2608_05448_amd import dblast as D
     wl = synth.WORKLOADS["qwen3_8b"]
     print(f"[fullsize] qwen3_8b e2e B={wl.B} K={wl.K} R={wl.R} d={wl.d} V={wl.V}", flush=True)
@@ -55,45 +60,42 @@ def test_e2e_qwen3_8b_sampled_blocks_all_temperatures():
     tls, lmass, lse = D.dbl_head_logprobs(h, w)
     z, x = D.dbl_sample_block(tls, lmass, lse, ell, z_temp=wl.z_temp, seed=wl.philox_seed, step=0)
     torch.cuda.synchronize()
-    blocks = [0, 9, 15]
-    w_np = np32(w)
+    B, K, R, V = wl.B, wl.K, wl.R, wl.V
+    print(f"[fullsize] qwen3_8b: oracle head on all {wl.M} rows", flush=True)
+    lq_all = oracle_full_head("qwen3_8b", h, w).reshape(B, K, R, V)
     z_g, x_g = z.cpu().numpy(), x.cpu().numpy()
     ell_np = ell.cpu().numpy()
-    lq_o = {b: _oracle_lq(h[b], w_np) for b in blocks}
+    z_o, x_o = MX.sample_blocks(lq_all, ell_np, wl.z_temp, wl.philox_seed, 0, np.arange(B))
+    np.testing.assert_array_equal(z_g, z_o)
     mismatches = 0
-    x_o = {}
-    for b in blocks:
-        zo, xo = MX.sample_blocks(lq_o[b][None], ell_np[b:b + 1], wl.z_temp, wl.philox_seed, 0,
-                                  np.array([b]))
-        assert z_g[b] == zo[0]
-        x_o[b] = xo
-        for k in range(wl.K):
-            if x_g[b, k] != xo[0, k]:
+    for b in range(B):
+        for k in range(K):
+            if x_g[b, k] != x_o[b, k]:
                 r = C.draw_u32(wl.philox_seed, C.PURPOSE_TOKEN, k, b, 0)
-                assert _near_tie_token(lq_o[b][k, zo[0]], r, x_g[b, k], xo[0, k])
+                assert _near_tie_token(lq_all[b, k, z_o[b]], r, x_g[b, k], x_o[b, k])
                 mismatches += 1
     print(f"[fullsize] qwen3_8b draw: certified near-ties {mismatches}", flush=True)
     # Verification is compared where both sides drafted the same block (all of them unless a
     # certified near-tie moved a token); each side verifies its own draft.
-    same = [b for b in blocks if np.array_equal(x_g[b], x_o[b][0])]
-    assert len(same) >= len(blocks) - mismatches
+    same = [b for b in range(B) if np.array_equal(x_g[b], x_o[b])]
+    assert len(same) >= B - mismatches
+    sel = np.array(same)
     for T in synth.QWEN3_8B_TEMPERATURES:
         logp = synth.make_logp(wl, rows=wl.K + 1, device="cuda", temperature=T)
         out = D.dbl_verify_block(tls, lmass, lse, ell, x, logp, z_temp=wl.z_temp,
                                  seed=wl.philox_seed, step=0)
         torch.cuda.synchronize()
         lp = logp.cpu().numpy()
-        for b in same:
-            ref = MX.verify_blocks(lq_o[b][None], ell_np[b:b + 1], wl.z_temp, x_o[b],
-                                   lp[b:b + 1], wl.philox_seed, 0, np.array([b]))
-            assert out["n_accept"][b].item() == ref["n_accept"][0]
-            assert out["next_token"][b].item() == ref["next_token"][0]
-            assert _rel(out["accept_mass"][b].cpu().numpy(), ref["beta"][0]) < 1e-4
-            assert _rel([out["exp_len"][b].item()], ref["E"]) < 1e-4
-            assert _rel([out["al_expected"][b].item()], ref["al"]) < 1e-4
+        ref = MX.verify_blocks(lq_all[sel], ell_np[sel], wl.z_temp, x_o[sel], lp[sel],
+                               wl.philox_seed, 0, sel)
+        np.testing.assert_array_equal(out["n_accept"].cpu().numpy()[sel], ref["n_accept"])
+        np.testing.assert_array_equal(out["next_token"].cpu().numpy()[sel], ref["next_token"])
+        assert _rel(out["accept_mass"].cpu().numpy()[sel], ref["beta"]) < 1e-4
+        assert _rel(out["exp_len"].cpu().numpy()[sel], ref["E"]) < 1e-4
+        assert _rel(out["al_expected"].cpu().numpy()[sel], ref["al"]) < 1e-4
         na = out["n_accept"].float().mean().item()
-        print(f"[fullsize] qwen3_8b T={T}: mean n_accept {na:.3f}, mean E "
-              f"{out['exp_len'].mean().item():.4f}", flush=True)
+        print(f"[fullsize] qwen3_8b T={T}: {len(same)} blocks match; mean n_accept {na:.3f}, "
+              f"mean E {out['exp_len'].mean().item():.4f}", flush=True)
 
 
 def test_objective_workload_chunked_expected_length():

@@ -107,6 +107,10 @@ GREEDY_CASES = [
     ("ragged-vocab", 4, 5, 6, 1001, 1.0, 5, 3, 7, 1, True, True),
     ("max-categories", 3, 4, 64, 700, 1.0, 6, 0, 0, 1, True, True),
     ("many-blocks", 96, 8, 4, 2000, 1.0, 7, 9, 4321, 1, True, True),
+    # The chain stages its gathers in LDS only for K <= 64 and K * R <= 1024; these two take the
+    # unstaged walk (K * R > 1024, and K > 64).
+    ("unstaged-wide", 4, 20, 64, 800, 1.0, 8, 0, 0, 1, True, True),
+    ("unstaged-long", 3, 80, 4, 600, 1.0, 9, 2, 0, 1, True, True),
 ]
 
 
