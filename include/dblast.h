@@ -199,6 +199,26 @@ dbl_status dbl_verify_block(dbl_shape shape, const float* tls, const float* lmas
                             float* exp_len, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * dbl_verify_block_static - dbl_verify_block for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * arguments without the workspace, the same kernels and bit-identical outputs. Its scratch is a
+ * fixed device array inside the library of 8 MiB (8388608 bytes), one copy per GPU, kept until
+ * the process ends; the call allocates and frees nothing. Limit: shapes whose verification
+ * workspace, dbl_workspace_bytes(DBL_OP_VERIFY, shape), exceeds 8 MiB are rejected (the
+ * Qwen3-8B step needs 0.36 MiB, B = 256 blocks of K = 8 at V = 151,936 need 5.2 MiB).
+ * Every call on one GPU shares that GPU's array: calls that overlap in time on one GPU (other
+ * streams, other threads) race and must not be issued; calls ordered on one stream are safe.
+ * `stream` must belong to the current device. Errors: as dbl_verify_block, plus DBL_EWORKSPACE
+ * for a shape beyond the fixed scratch and DBL_EINVAL for a stream of another device.
+ */
+dbl_status dbl_verify_block_static(dbl_shape shape, const float* tls, const float* lmass,
+                                   const float* lse, const float* prior_logits, float z_temp,
+                                   const int32_t* x, const float* logp, int64_t Kp,
+                                   uint64_t seed, uint64_t step, int64_t seq_offset,
+                                   int32_t* n_accept, int32_t* next_token, float* accept_mass,
+                                   float* al_expected, float* exp_len, void* stream);
+
+/*
  * dbl_expected_len - the expected-accepted-length reduction that the acceptance-oriented
  * objective targets (Sec. "Acceptance-Oriented Training"): along a given trajectory x (for
  * example one drawn from the target), beta_k = sum_v min(p_k(v), q_k(v | x_<k)) with the

@@ -6,6 +6,7 @@
 
 #include <cstdio>
 #include <initializer_list>
+#include <mutex>
 #include <string>
 
 #include "../../include/dblast.h"
@@ -179,6 +180,83 @@ dbl::GreedyArgs greedy_args(const dbl_shape& s, const int32_t* xhat, const float
   return a;
 }
 
+// Argument checks of the two verification entry points.
+dbl_status check_verify(const dbl_shape& s, const float* tls, const float* lmass,
+                        const float* lse, const float* prior_logits, float z_temp,
+                        const int32_t* x, const float* logp, int64_t Kp, int32_t* n_accept,
+                        int32_t* next_token, float* accept_mass, float* al_expected,
+                        float* exp_len) {
+  if (dbl_status st = check_block_inputs(s, tls, lmass, lse, prior_logits, z_temp)) return st;
+  if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
+  if (!n_accept || !next_token) return fail(DBL_EINVAL, "NULL output pointer");
+  if (Kp != s.K && Kp != s.K + 1) return fail(DBL_EINVAL, "Kp must be K or K + 1");
+  return check_aligned({{x, "x"}, {logp, "logp"}, {n_accept, "n_accept"},
+                        {next_token, "next_token"}, {accept_mass, "accept_mass"},
+                        {al_expected, "al_expected"}, {exp_len, "exp_len"}});
+}
+
+// Verification launch with its scratch carved out of `base` (a caller workspace or the fixed
+// scratch) by the DBL_OP_VERIFY layout.
+dbl_status launch_verify_in(const dbl_shape& s, const float* tls, const float* lmass,
+                            const float* lse, const float* prior_logits, float z_temp,
+                            const int32_t* x, const float* logp, int64_t Kp, uint64_t seed,
+                            uint64_t step, int64_t seq_offset, int32_t* n_accept,
+                            int32_t* next_token, float* accept_mass, float* al_expected,
+                            float* exp_len, char* base, const WsLayout& L, void* stream) {
+  dbl::VerifyArgs a;
+  a.blk = block_args(s, tls, lmass, lse, prior_logits, z_temp, seed, step, seq_offset);
+  a.x = x;
+  a.logp = logp;
+  a.Kp = Kp;
+  a.trajectory = false;
+  a.n_accept = n_accept;
+  a.next_token = next_token;
+  a.beta = accept_mass;
+  a.al = al_expected;
+  a.exp_len = exp_len;
+  a.wpost = reinterpret_cast<double*>(base + L.off[0]);
+  a.beta_part = reinterpret_cast<float*>(base + L.off[1]);
+  a.res_tiles = reinterpret_cast<uint64_t*>(base + L.off[2]);
+  a.p_tiles = reinterpret_cast<uint64_t*>(base + L.off[3]);
+  return hip_status(dbl::launch_verify(a, static_cast<hipStream_t>(stream)), "verify launch");
+}
+
+// Scratch of dbl_verify_block_static, for callers that cannot allocate: a fixed device array,
+// one copy per GPU, held until the process ends. Its name is a host-side stand-in, never a
+// device address: each device's address is resolved once, with that device current, by
+// hipGetSymbolAddress, and only that address is handed to kernels. Every kernel writes the
+// parts it reads before reading them, so nothing needs clearing between calls.
+constexpr size_t kStaticScratchBytes = size_t(8) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+dbl_status static_scratch(void* stream, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(DBL_EHIP, "device index out of range");
+  if (stream) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev);
+    if (e != hipSuccess) return hip_status(e, "hipStreamGetDevice");
+    if (sdev != dev) return fail(DBL_EINVAL, "stream belongs to a device other than the current one");
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p || reinterpret_cast<uintptr_t>(p) % 256 != 0)
+      return fail(DBL_EHIP, "fixed scratch has no 256-byte aligned device address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -260,34 +338,37 @@ dbl_status dbl_verify_block(dbl_shape s, const float* tls, const float* lmass,
                             uint64_t step, int64_t seq_offset, int32_t* n_accept,
                             int32_t* next_token, float* accept_mass, float* al_expected,
                             float* exp_len, void* ws, size_t ws_bytes, void* stream) {
-  if (dbl_status st = check_block_inputs(s, tls, lmass, lse, prior_logits, z_temp)) return st;
-  if (!x || !logp) return fail(DBL_EINVAL, "NULL input pointer");
-  if (!n_accept || !next_token) return fail(DBL_EINVAL, "NULL output pointer");
-  if (Kp != s.K && Kp != s.K + 1) return fail(DBL_EINVAL, "Kp must be K or K + 1");
-  if (dbl_status st = check_aligned({{x, "x"}, {logp, "logp"}, {n_accept, "n_accept"},
-                                     {next_token, "next_token"}, {accept_mass, "accept_mass"},
-                                     {al_expected, "al_expected"}, {exp_len, "exp_len"}}))
+  if (dbl_status st = check_verify(s, tls, lmass, lse, prior_logits, z_temp, x, logp, Kp,
+                                   n_accept, next_token, accept_mass, al_expected, exp_len))
     return st;
   WsLayout L;
   if (dbl_status st = check_ws(DBL_OP_VERIFY, s, ws, ws_bytes, &L)) return st;
   if (s.B == 0) return ok();
-  char* base = static_cast<char*>(ws);
-  dbl::VerifyArgs a;
-  a.blk = block_args(s, tls, lmass, lse, prior_logits, z_temp, seed, step, seq_offset);
-  a.x = x;
-  a.logp = logp;
-  a.Kp = Kp;
-  a.trajectory = false;
-  a.n_accept = n_accept;
-  a.next_token = next_token;
-  a.beta = accept_mass;
-  a.al = al_expected;
-  a.exp_len = exp_len;
-  a.wpost = reinterpret_cast<double*>(base + L.off[0]);
-  a.beta_part = reinterpret_cast<float*>(base + L.off[1]);
-  a.res_tiles = reinterpret_cast<uint64_t*>(base + L.off[2]);
-  a.p_tiles = reinterpret_cast<uint64_t*>(base + L.off[3]);
-  return hip_status(dbl::launch_verify(a, static_cast<hipStream_t>(stream)), "verify launch");
+  return launch_verify_in(s, tls, lmass, lse, prior_logits, z_temp, x, logp, Kp, seed, step,
+                          seq_offset, n_accept, next_token, accept_mass, al_expected, exp_len,
+                          static_cast<char*>(ws), L, stream);
+}
+
+dbl_status dbl_verify_block_static(dbl_shape s, const float* tls, const float* lmass,
+                                   const float* lse, const float* prior_logits, float z_temp,
+                                   const int32_t* x, const float* logp, int64_t Kp,
+                                   uint64_t seed, uint64_t step, int64_t seq_offset,
+                                   int32_t* n_accept, int32_t* next_token, float* accept_mass,
+                                   float* al_expected, float* exp_len, void* stream) {
+  if (dbl_status st = check_verify(s, tls, lmass, lse, prior_logits, z_temp, x, logp, Kp,
+                                   n_accept, next_token, accept_mass, al_expected, exp_len))
+    return st;
+  const WsLayout L = layout(DBL_OP_VERIFY, s);
+  if (L.total > kStaticScratchBytes)
+    return fail(DBL_EWORKSPACE, "this shape needs " + std::to_string(L.total) +
+                                    " bytes of scratch; the fixed scratch holds " +
+                                    std::to_string(kStaticScratchBytes));
+  if (s.B == 0) return ok();
+  void* base = nullptr;
+  if (dbl_status st = static_scratch(stream, &base)) return st;
+  return launch_verify_in(s, tls, lmass, lse, prior_logits, z_temp, x, logp, Kp, seed, step,
+                          seq_offset, n_accept, next_token, accept_mass, al_expected, exp_len,
+                          static_cast<char*>(base), L, stream);
 }
 
 dbl_status dbl_expected_len(dbl_shape s, const float* tls, const float* lmass,

@@ -52,6 +52,8 @@ _SIGS = {
                                         _SZ, _P]),
     "dbl_verify_block": (ctypes.c_int, [Shape, _P, _P, _P, _P, _F, _P, _P, _I64, _U64, _U64, _I64,
                                         _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "dbl_verify_block_static": (ctypes.c_int, [Shape, _P, _P, _P, _P, _F, _P, _P, _I64, _U64,
+                                               _U64, _I64, _P, _P, _P, _P, _P, _P]),
     "dbl_expected_len": (ctypes.c_int, [Shape, _P, _P, _P, _P, _F, _P, _P, _P, _P, _P, _SZ, _P]),
     "dbl_sample_greedy": (ctypes.c_int, [Shape, _P, _P, _F, _U64, _U64, _I64, _P, _P, _P]),
     "dbl_verify_greedy": (ctypes.c_int, [Shape, _P, _P, _F, _P, _P, _I64, _U64, _U64, _I64, _P,
@@ -225,6 +227,37 @@ def dbl_verify_block(tls, lmass, lse, prior_logits, x, logp, z_temp=1.0, seed=0,
                                    _ptr(o["next_token"]), _ptr(o.get("accept_mass")),
                                    _ptr(o.get("al_expected")), _ptr(o.get("exp_len")), _ptr(ws),
                                    nws, _stream(dev)))
+    return o
+
+
+def dbl_verify_block_static(tls, lmass, lse, prior_logits, x, logp, z_temp=1.0, seed=0, step=0,
+                            seq_offset=0, want_beta=True, want_al=True, want_exp_len=True,
+                            out=None):
+    """``dbl_verify_block`` without a workspace: the library's fixed per-GPU scratch is used
+    (shapes needing more than 8 MiB of it are rejected). Calls that overlap on one GPU race."""
+    shape = _block_shape(tls, lmass, lse, prior_logits)
+    dev = tls.device
+    B, K, V = shape.B, shape.K, shape.V
+    _need(x, "x", torch.int32, (B, K))
+    if logp.dim() != 3 or logp.shape[0] != B or logp.shape[2] != V:
+        raise ValueError("logp must be [B, Kp, V]")
+    _need(logp, "logp", torch.float32)
+    Kp = logp.shape[1]
+    o = {} if out is None else dict(out)
+    o.setdefault("n_accept", torch.empty(B, dtype=torch.int32, device=dev))
+    o.setdefault("next_token", torch.empty(B, dtype=torch.int32, device=dev))
+    if want_beta:
+        o.setdefault("accept_mass", torch.empty((B, K), dtype=torch.float32, device=dev))
+    if want_al:
+        o.setdefault("al_expected", torch.empty(B, dtype=torch.float32, device=dev))
+    if want_exp_len:
+        o.setdefault("exp_len", torch.empty(B, dtype=torch.float32, device=dev))
+    _check(load().dbl_verify_block_static(shape, _ptr(tls), _ptr(lmass), _ptr(lse),
+                                          _ptr(prior_logits), float(z_temp), _ptr(x), _ptr(logp),
+                                          int(Kp), int(seed), int(step), int(seq_offset),
+                                          _ptr(o["n_accept"]), _ptr(o["next_token"]),
+                                          _ptr(o.get("accept_mass")), _ptr(o.get("al_expected")),
+                                          _ptr(o.get("exp_len")), _stream(dev)))
     return o
 
 

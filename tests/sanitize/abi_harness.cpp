@@ -157,6 +157,27 @@ int main(int argc, char** argv) {
                          nullptr, nullptr, 0, null) == DBL_OK);
   CHECK(g_launches == before);
 
+  // --- the allocation-free verification: rejections happen before any runtime call ---------
+  before = g_launches;
+  {
+    dbl_shape big{1024, 16, 8, 0, 151936};  // needs ~19 MiB of scratch
+    CHECK(dbl_workspace_bytes(DBL_OP_VERIFY, big) > (size_t(8) << 20));
+    CHECK(dbl_verify_block_static(big, F(a(0)), F(a(1)), F(a(2)), F(a(3)), 1.0f, I(a(4)),
+                                  F(a(5)), 16, 0, 0, 0, I(a(6)), I(a(7)), nullptr, nullptr,
+                                  nullptr, null) == DBL_EWORKSPACE);
+    CHECK(strstr(dbl_last_error(), "fixed scratch") != nullptr);
+    CHECK(dbl_verify_block_static(bs, F(a(0)), F(a(1)), F(a(2)), F(a(3)), 1.0f, I(a(4)),
+                                  F(a(5)) + 1, 7, 0, 0, 0, I(a(6)), I(a(7)), nullptr, nullptr,
+                                  nullptr, null) == DBL_EINVAL);
+    CHECK(dbl_verify_block_static(bs, F(a(0)), F(a(1)), F(a(2)), F(a(3)), 1.0f, I(a(4)),
+                                  F(a(5)), 6, 0, 0, 0, I(a(6)), I(a(7)), nullptr, nullptr,
+                                  nullptr, null) == DBL_EINVAL);
+    CHECK(dbl_verify_block_static(dbl_shape{0, 7, 3, 0, 100}, F(a(0)), F(a(1)), F(a(2)),
+                                  F(a(3)), 1.0f, I(a(4)), F(a(5)), 7, 0, 0, 0, I(a(6)), I(a(7)),
+                                  nullptr, nullptr, nullptr, null) == DBL_OK);
+  }
+  CHECK(g_launches == before);
+
   // --- greedy ------------------------------------------------------------------------------
   CHECK(dbl_sample_greedy(bs, I(a(0)), F(a(1)), 0.0f, 1, 2, 3, I(a(2)), I(a(3)), null) ==
         DBL_OK);

@@ -306,3 +306,24 @@ def test_hidden_size_cap(lib):
     assert lib.dbl_workspace_bytes(D.DBL_OP_HEAD, S(1, 1, 1, 1 << 23, 256)) == \
         ctypes.c_size_t(-1).value
     assert lib.dbl_workspace_bytes(D.DBL_OP_HEAD, S(1, 1, 1, 1 << 20, 256)) == 256  # 8, rounded up
+
+
+def test_static_verify_rejects_shapes_beyond_its_scratch(lib):
+    """dbl_verify_block_static has a fixed 8 MiB scratch: a shape that needs more is
+    DBL_EWORKSPACE before anything is launched; invalid arguments fail as in dbl_verify_block."""
+    S = D.Shape
+    p = _fake(10)
+    null = ctypes.c_void_p(None)
+    big = S(1024, 16, 8, 0, 151936)
+    assert lib.dbl_workspace_bytes(D.DBL_OP_VERIFY, big) > 8 << 20
+    assert lib.dbl_verify_block_static(big, p[0], p[1], p[2], p[3], 1.0, p[4], p[5], 16, 0, 0,
+                                       0, p[6], p[7], null, null, null, null) == D.DBL_EWORKSPACE
+    assert "fixed scratch" in _err(lib)
+    shape = S(2, 4, 3, 0, 300)
+    for kp in (3, 6):
+        assert lib.dbl_verify_block_static(shape, p[0], p[1], p[2], p[3], 1.0, p[4], p[5], kp, 0,
+                                           0, 0, p[6], p[7], null, null, null,
+                                           null) == D.DBL_EINVAL
+    assert lib.dbl_verify_block_static(S(0, 4, 3, 0, 300), p[0], p[1], p[2], p[3], 1.0, p[4],
+                                       p[5], 4, 0, 0, 0, p[6], p[7], null, null, null,
+                                       null) == D.DBL_OK

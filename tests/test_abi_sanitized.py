@@ -24,9 +24,9 @@ def _tools():
 
 def test_abi_validation_layer_is_clean_under_asan_and_ubsan(tmp_path):
     hipcc, clang = _tools()
-    # Host-only compiles: the sanitizer flags apply to the host pass alone.
+    # The sanitizer flags apply to the host pass alone (-Xarch_host); device code is unchanged.
     flags = ["-O1", "-g", "-fno-omit-frame-pointer", "-std=c++17", "--offload-arch=gfx950",
-             "--cuda-host-only", "-Xarch_host", "-fsanitize=address", "-Xarch_host",
+             "-Xarch_host", "-fsanitize=address", "-Xarch_host",
              "-fsanitize=undefined", "-Xarch_host", "-fno-sanitize-recover=undefined",
              f"-I{os.path.join(ROOT, 'include')}"]
     objs = []
