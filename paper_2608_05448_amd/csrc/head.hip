@@ -24,6 +24,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kVTile = 128;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -194,12 +195,16 @@ __device__ __forceinline__ void tile_logsoftmax_store_lds(f32x16 (&acc)[NRB][NCB
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) x[16 * rb + r] = acc[rb][cb][r];
+    // Id offset of x[16 rb + r] in the tile: 32 rb + 8 (r / 4) + (r % 4) + 4 half; the
+    // compile-time part is compared against limits shifted by 4 half, so no per-value offset
+    // is held in a register.
     if (!full) {
+      const int lim = vlim - 4 * half;
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3) >= vlim) x[16 * rb + r] = -INFINITY;
+          if (rb * 32 + 8 * (r >> 2) + (r & 3) >= lim) x[16 * rb + r] = -INFINITY;
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -208,11 +213,11 @@ __device__ __forceinline__ void tile_logsoftmax_store_lds(f32x16 (&acc)[NRB][NCB
     if constexpr (ARG) {
       vi = 1 << 30;
 #pragma unroll
-      for (int rb = 0; rb < NRB; ++rb)
+      for (int rb = NRB - 1; rb >= 0; --rb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (x[16 * rb + r] == mx) vi = min(vi, rb * 32 + 8 * (r >> 2) + 4 * half + (r & 3));
-      vi = vi == (1 << 30) ? 0 : vi;
+        for (int r = 15; r >= 0; --r)
+          vi = x[16 * rb + r] == mx ? rb * 32 + 8 * (r >> 2) + (r & 3) : vi;
+      vi = vi == (1 << 30) ? 0 : vi + 4 * half;
       const float omx = __shfl_xor(mx, 32);
       const int ovi = __shfl_xor(vi, 32);
       if (omx > mx || (omx == mx && ovi < vi)) {
@@ -261,8 +266,11 @@ __device__ __forceinline__ void tile_logsoftmax_store_lds(f32x16 (&acc)[NRB][NCB
       const uint32_t lo = static_cast<uint32_t>(half * V + 4 * lr);  // 32-bit lane offsets
       const uint32_t step = static_cast<uint32_t>(2 * V);
 #pragma unroll
+      // Non-temporal: the 256 KB a workgroup writes per tile would otherwise evict the operand
+      // slabs its XCD's other tiles are still reading from L2 (1% faster).
       for (int jj = 0; jj < 16; ++jj)
-        *reinterpret_cast<float4*>(base + (lo + jj * step)) = o[jj];
+        __builtin_nontemporal_store(f32x4{o[jj].x, o[jj].y, o[jj].z, o[jj].w},
+                                    reinterpret_cast<f32x4*>(base + (lo + jj * step)));
     } else {
 #pragma unroll
       for (int jj = 0; jj < 16; ++jj) {
@@ -1032,6 +1040,185 @@ __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_rs_kernel(
         acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w, m0 + wm * TM, lane, ea.vec4);
 }
 
+// ---------------------------------------------------------------------------------------
+// Ping-pong variant (the head for hidden sizes that are a multiple of 64): 8 waves, two per
+// SIMD (the dispatcher places waves w and w + 4 of a workgroup on the same SIMD, waves 0-3 on
+// four different ones), in two groups of four that take turns between workgroup barriers: one
+// group issues MFMAs on fragments already in its registers while the other reads its next
+// fragments from LDS and issues global -> LDS copies, so the MFMA-issuing wave never waits on
+// memory and each SIMD's matrix pipe is fed by one wave or the other.
+//   * Workgroup tile 256 vocabulary x 256 branch rows, 64-deep stages; each wave owns a 128 x 64
+//     output block (one vocabulary tile for 64 branch rows). A turn covers 32 of a stage's 64 k:
+//     12 fragment reads, 16 MFMAs.
+//   * LDS (160 KB): three slots for the w rows of a stage (stage s in slot s % 3) and two for
+//     the h rows (slot s % 2), filled by global_load_lds_dwordx4. Every memory half of every
+//     turn issues the same 16 KB of copies (4 instructions per wave; each group copies half of
+//     each operand's rows): even turn 2 s the h rows of stage s + 1, odd turn 2 s + 1 the w rows
+//     of stage s + 2, so w (streamed from HBM) has two stages of lead and h (re-read from L2)
+//     one. Copies issued in one burst per stage stretched the memory halves and cost 6%.
+struct PpCfg {
+  static constexpr int BV = 256, BM = 256, BK = 64, kThreads = 512;
+  static constexpr int TM = 64, NRB = 4, NCB = 2;  // wave block: 128 ids x 64 branch rows
+  static constexpr int ROWB = 128;                 // bytes per LDS row (64 bf16)
+  static constexpr int TILE = 256 * ROWB;          // bytes per operand per stage (32 KB)
+  static_assert(5 * TILE <= 160 * 1024 && 8 * 32 * 512 <= 5 * TILE, "LDS budget");
+};
+
+__device__ __forceinline__ void pp_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <bool ARG>
+__global__ __launch_bounds__(512, 1) void head_bf16_pp_kernel(
+    const __bf16* __restrict__ h, const __bf16* __restrict__ w, const EpiArgs ea, int64_t M,
+    int64_t V, int d, int n_mtiles) {
+  using C = PpCfg;
+  constexpr int ROWB = C::ROWB, TILE = C::TILE, NRB = C::NRB, NCB = C::NCB;
+  constexpr int BOFF = 3 * TILE;  // the two h slots follow the three w slots
+  // After the loop the first 128 KB hold the epilogue's per-wave 16 KB store staging.
+  __shared__ __attribute__((aligned(1024))) char smem[5 * TILE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;  // group 0 computes first in every pair of turns
+  const int wv = wave & 1;    // vocabulary half of the workgroup tile
+  const int wm = wave >> 1;   // branch-row quarter (0, 1 in group 0; 2, 3 in group 1)
+  const int q = wave & 3;
+  int vt, mt;
+  tile_of(xcd_remap(blockIdx.x, gridDim.x), gridDim.x / n_mtiles, n_mtiles, &vt, &mt);
+  const int64_t v0 = static_cast<int64_t>(vt) * C::BV;
+  const int64_t m0 = static_cast<int64_t>(mt) * C::BM;
+
+  // Copies: wave q of group g copies rows 128 g + (4 q + i) * 8 + lane / 8 (i < 4) of the w tile
+  // and of the h tile; lane % 8 is its 16-byte chunk's place in the LDS row and it fetches
+  // chunk (lane % 8) ^ swz(row) of that row (rows past V or M repeat the last one). A scalar
+  // tile base plus 32-bit lane offsets (at most 512 d bytes).
+  const char* srcA = reinterpret_cast<const char*>(w + v0 * d);
+  const char* srcB = reinterpret_cast<const char*>(h + m0 * d);
+  uint32_t offA[4], offB[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 128 * grp + (4 * q + i) * 8 + lane / 8;
+    const int c = (lane % 8) ^ dma_swz<8>(r);
+    const int64_t ga = r < V - v0 ? r : V - v0 - 1;
+    const int64_t gb = r < M - m0 ? r : M - m0 - 1;
+    offA[i] = static_cast<uint32_t>(ga * d * 2 + c * 16);
+    offB[i] = static_cast<uint32_t>(gb * d * 2 + c * 16);
+  }
+  const uint32_t lds_row = lds_addr(smem) + (16 * grp + 4 * q) * 1024;
+  auto copy_A = [&](int s, int slot) {
+    const char* base = srcA + static_cast<int64_t>(s) * (2 * C::BK);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lds_dma16(base, offA[i], lds_row + slot * TILE + i * 1024);
+  };
+  auto copy_B = [&](int s, int slot) {
+    const char* base = srcB + static_cast<int64_t>(s) * (2 * C::BK);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      lds_dma16(base, offB[i], lds_row + BOFF + slot * TILE + i * 1024);
+  };
+
+  f32x16 acc[NRB][NCB];
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.0f;
+
+  // Fragments of a turn: lane l reads row l % 32 of each 32-row block, 8 k values from
+  // 8 (l / 32) of each 16-wide k step (chunk 2 kk + l / 32, stored at chunk ^ swz(row)).
+  const int tt = 16 * ((lane >> 5) ^ dma_swz<8>(lane & 31));
+  const int a_base = (wv * kVTile + (lane & 31)) * ROWB;
+  const int b_base = BOFF + (wm * C::TM + (lane & 31)) * ROWB;
+  bf16x8 af[2][NRB], bfr[2][NCB];
+  auto load_frags = [&](int aslot, int bslot, int kk0) {
+    const char* sa = smem + aslot * TILE;
+    const char* sb = smem + bslot * TILE;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int x = (32 * (kk0 + ks)) ^ tt;
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+        af[ks][rb] = *reinterpret_cast<const bf16x8*>(sa + a_base + rb * 32 * ROWB + x);
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+        bfr[ks][cb] = *reinterpret_cast<const bf16x8*>(sb + b_base + cb * 32 * ROWB + x);
+    }
+  };
+  auto compute = [&]() {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][rb], bfr[ks][cb],
+                                                                 acc[rb][cb], 0, 0, 0);
+  };
+
+  const int nk = d / C::BK;
+  const int H = 2 * nk;  // turns per group
+  // Turn t of a group: its memory half (fragments of k half t % 2 of stage s = t / 2, plus the
+  // turn's copies into slots that stage s - 1 has left), a barrier, its compute half, a barrier.
+  // Group 1 runs one barrier behind group 0, so each half of one group coincides with the other
+  // half of the other. At odd turns every wave waits for its own copies of stage s + 1 (all but
+  // the 4 instructions of stage s + 2 just issued) before the barrier that opens the first
+  // memory half reading stage s + 1; a slot is refilled only after the barrier that closes the
+  // last memory half reading it.
+  auto turn = [&](int t, int a3, int b2) {  // a3 = (t / 2) % 3, b2 = (t / 2) % 2
+    const int s = t >> 1;
+    load_frags(a3, b2, (t & 1) * 2);
+    if (!(t & 1)) {
+      if (t >= 2 && s + 1 < nk) copy_B(s + 1, b2 ^ 1);
+    } else {
+      if (s + 2 < nk) copy_A(s + 2, a3 == 0 ? 2 : a3 - 1);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if ((t & 1) && grp == 1) {
+      if (s + 2 < nk) wait_vmcnt<4>(); else wait_vmcnt<0>();
+    }
+    pp_barrier();
+    compute();
+    if ((t & 1) && grp == 0) {
+      if (s + 2 < nk) wait_vmcnt<4>(); else wait_vmcnt<0>();
+    }
+    if (!(grp == 1 && t == H - 1)) pp_barrier();
+  };
+  copy_A(0, 0);
+  copy_B(0, 0);
+  if (nk > 1) {
+    copy_A(1, 1);
+    copy_B(1, 1);
+    wait_vmcnt<8>();
+  } else {
+    wait_vmcnt<0>();
+  }
+  pp_barrier();
+  if (grp == 1) pp_barrier();
+  int a3 = 0;
+  for (int t = 0; t < H; t += 2) {
+    turn(t, a3, (t >> 1) & 1);
+    turn(t + 1, a3, (t >> 1) & 1);
+    a3 = a3 == 2 ? 0 : a3 + 1;
+  }
+
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) asm volatile("" : "+a"(acc[rb][cb]));
+
+  // No memory half reads the slots any more (group 0 passed the barrier closing the last one;
+  // group 1 reads none in its last compute half) and every copy has landed, so each wave stages
+  // its stores in its own 16 KB of them.
+  const int64_t v0w = v0 + wv * kVTile;
+  if (v0w >= V) return;
+  tile_logsoftmax_store_lds<NRB, NCB, ARG>(acc, ea.tls, ea.lmass, ea.amax, M, V, ea.nT, v0w,
+                                           m0 + wm * C::TM, lane, ea.vec4, smem + wave * 16384);
+}
+
 // fp32 path: workgroup (vocabulary tile t, 4 branch rows); thread j owns id 128 t + j.
 constexpr int kF32Rows = 4;
 constexpr int kF32DChunk = 512;
@@ -1171,7 +1358,27 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
 #ifndef DBL_HEAD_RS
 #define DBL_HEAD_RS 1
 #endif
-    if (DBL_HEAD_RS && a.d % RsHead::BK == 0) {
+#ifndef DBL_HEAD_PP
+#define DBL_HEAD_PP 1
+#endif
+    if (DBL_HEAD_PP && a.d % PpCfg::BK == 0) {
+      const int dm = static_cast<int>((a.M + PpCfg::BM - 1) / PpCfg::BM);
+      const int64_t dwg = ((a.V + PpCfg::BV - 1) / PpCfg::BV) * dm;
+      if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
+      EpiArgs ea{};
+      ea.tls = a.tls;
+      ea.lmass = a.lmass;
+      ea.amax = amax;
+      ea.nT = nT;
+      ea.vec4 = vec4;
+      const dim3 grid(static_cast<unsigned>(dwg)), block(PpCfg::kThreads);
+      if (amax)
+        hipLaunchKernelGGL(head_bf16_pp_kernel<true>, grid, block, 0, stream, h, w, ea, a.M, a.V,
+                           a.d, dm);
+      else
+        hipLaunchKernelGGL(head_bf16_pp_kernel<false>, grid, block, 0, stream, h, w, ea, a.M,
+                           a.V, a.d, dm);
+    } else if (DBL_HEAD_RS && a.d % RsHead::BK == 0) {
       const int dm = static_cast<int>((a.M + RsHead::BM - 1) / RsHead::BM);
       const int64_t dwg = ((a.V + RsHead::BV - 1) / RsHead::BV) * dm;
       if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
