@@ -15,6 +15,10 @@
 //             the bonus row when every position was accepted.
 //   finalize  one 256-thread workgroup per block: acceptance masses,
 //             E = sum_i prod_{j<=i} beta_j, and the residual/bonus inverse-CDF draw.
+//   stream    (V % 4 == 0, masses requested: the usual case) beta, residual and finalize in one
+//             launch after the chain: the residual's tile sums come from the stream's own loads
+//             at the first rejected position, and the last of a block's workgroups to finish
+//             finalises it.
 // The same kernels serve the expected-length reduction along a given trajectory (no accept
 // test, no residual). Built with floating-point contraction off (determinism contract).
 #include <hip/hip_runtime.h>
@@ -33,6 +37,7 @@ __global__ __launch_bounds__(64) void chain_kernel(VerifyArgs a) {
   const BlockArgs& k_ = a.blk;
   const int64_t b = blockIdx.x;
   const int lane = lane_id();
+  if (a.arrive && lane == 0) a.arrive[b] = 0;  // read by the next launch's stream workgroups
   const int R = static_cast<int>(k_.R);
   const uint64_t seq = static_cast<uint64_t>(k_.seq_offset + b);
   double L = prior_log_weight(k_.prior + b * k_.R, R, k_.z_temp);
@@ -90,6 +95,7 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
   const int K = static_cast<int>(k_.K);
   const int KR = K * R;
   const uint64_t seq = static_cast<uint64_t>(k_.seq_offset + b);
+  if (a.arrive && tid == 0) a.arrive[b] = 0;  // read by the next launch's stream workgroups
   __shared__ float s_lq[kChainMaxKR];
   __shared__ double s_L[kChainMaxKR];
   __shared__ double s_L0[kMaxR];
@@ -421,14 +427,13 @@ __global__ __launch_bounds__(256) void beta_residual_kernel(VerifyArgs a) {
     beta_body<RT>(a, blockIdx.x - B, blockIdx.y, gridDim.y);
 }
 
-// Per block: acceptance masses and E (binary64 sums of the chunk partials), then the residual
-// or bonus draw by inverse CDF over the tile sums (256 threads).
-__global__ __launch_bounds__(256) void finalize_kernel(VerifyArgs a, int nchunk) {
+// Block b: acceptance masses and E (binary64 sums of the chunk partials), then the residual or
+// bonus draw by inverse CDF over the tile sums. Run by a whole 256-thread workgroup.
+__device__ void finalize_block(const VerifyArgs& a, int64_t b, int nchunk) {
   __shared__ double s_beta[kChainMaxK];
   __shared__ uint64_t lds[8];
   __shared__ double wz[kMaxR];
   const BlockArgs& k_ = a.blk;
-  const int64_t b = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
@@ -496,6 +501,172 @@ __global__ __launch_bounds__(256) void finalize_kernel(VerifyArgs a, int nchunk)
   if (tid == 0) a.next_token[b] = tok;
 }
 
+__global__ __launch_bounds__(256) void finalize_kernel(VerifyArgs a, int nchunk) {
+  finalize_block(a, blockIdx.x, nchunk);
+}
+
+// The acceptance-mass stream with the residual tile sums and the per-block finalisation folded
+// in (V % 4 == 0, masses requested). Workgroup g handles chunk c = g % nchunk (32 vocabulary
+// tiles) of position row k of block b, g / nchunk = k B + b:
+//  * k < K: the R branch rows and the target row of the chunk are read once for the
+//    acceptance-mass partial; at the block's first rejected position the same loaded values also
+//    give the contract's integer residual and target tile sums (weights as in residual_body), so
+//    no row is read twice;
+//  * k = K (rows of the bonus row, present when Kp = K + 1): read only when the block accepted
+//    every position, for the bonus row's integer tile sums.
+// Each workgroup then counts itself in its block's arrival counter (zeroed by the chain kernel
+// that precedes this launch); the last to arrive sees every partial of the block and finalises
+// it. Counting replaces the separate finalize launch; nothing waits on another workgroup.
+constexpr float kLog2eChunk = 1.4426950408889634f;
+
+// Eight waves per SIMD (64 VGPRs): the binary64 residual arithmetic, which only the workgroups
+// at a first rejection run, would otherwise set the register budget of every workgroup.
+template <int RT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
+  const BlockArgs& k_ = a.blk;
+  const int64_t B = k_.B;
+  const int c = static_cast<int>(blockIdx.x % static_cast<unsigned>(nchunk));
+  const int64_t pb = blockIdx.x / static_cast<unsigned>(nchunk);
+  const int64_t k = pb / B, b = pb % B;
+  const int R = RT > 0 ? RT : static_cast<int>(k_.R);
+  const int64_t V = k_.V;
+  const int tid = threadIdx.x;
+  __shared__ float s_w[kMaxR];
+  __shared__ double s_wz[kMaxR];
+  __shared__ float s_offx[kMaxR][kTilesPerChunk];  // fl32(lmass - lse) of the chunk's tiles
+  __shared__ float red[4];
+  __shared__ int s_last;
+  const int ks = a.trajectory ? -1 : a.n_accept[b];  // first rejected position, K if none
+  const bool bonus = k == k_.K;
+  const bool res = !a.trajectory && (bonus ? ks == k_.K : k == ks);
+  const int t0 = c * kTilesPerChunk;
+  const int nt = min(kTilesPerChunk, k_.nT - t0);
+  const int64_t m0 = (b * k_.K + k) * k_.R;  // first branch row of the position (k < K)
+  if (!bonus) {
+    for (int i = tid; i < R * kTilesPerChunk; i += blockDim.x) {
+      const int z = i / kTilesPerChunk, tt = i % kTilesPerChunk;
+      if (tt < nt) s_offx[z][tt] = k_.lmass[(m0 + z) * k_.nT + t0 + tt] - k_.lse[m0 + z];
+    }
+    if (tid < R) {
+      const double wv = a.wpost[m0 + tid];
+      s_w[tid] = static_cast<float>(wv);
+      s_wz[tid] = wv;
+    }
+  }
+  __syncthreads();
+  const int64_t vb = static_cast<int64_t>(t0) * kTile;
+  const int64_t ve = min(V, vb + static_cast<int64_t>(nt) * kTile);
+  const float* prow = a.logp + (b * a.Kp + k) * V;
+  const float* trow = k_.tls + m0 * V;
+  float acc = 0.0f;
+  if (!bonus || res) {
+#pragma unroll 1
+    for (int i = 0; i < kTilesPerChunk * kTile / 1024; ++i) {
+      const int64_t v = vb + 4 * tid + 1024 * i;
+      const int tt = (4 * tid + 1024 * i) >> 7;  // the 32 threads of a half-wave share a tile
+      uint64_t sp = 0, sr = 0;
+      if (v < ve) {
+        const float4 p = *reinterpret_cast<const float4*>(prow + v);
+        const float pe[4] = {p.x, p.y, p.z, p.w};
+        float4 x[RT > 0 ? RT : 1];
+        if (!bonus) {
+          float q0 = 0.0f, q1 = 0.0f, q2 = 0.0f, q3 = 0.0f;
+          if constexpr (RT > 0) {
+#pragma unroll
+            for (int z = 0; z < RT; ++z) x[z] = *reinterpret_cast<const float4*>(trow + z * V + v);
+#pragma unroll
+            for (int z = 0; z < RT; ++z) {
+              const float o = s_offx[z][tt] * kLog2eChunk, w = s_w[z];
+              q0 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(x[z].x, kLog2eChunk, o)), q0);
+              q1 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(x[z].y, kLog2eChunk, o)), q1);
+              q2 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(x[z].z, kLog2eChunk, o)), q2);
+              q3 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(x[z].w, kLog2eChunk, o)), q3);
+            }
+          } else {
+            for (int z = 0; z < R; ++z) {
+              const float4 xz = *reinterpret_cast<const float4*>(trow + z * V + v);
+              const float o = s_offx[z][tt] * kLog2eChunk, w = s_w[z];
+              q0 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.x, kLog2eChunk, o)), q0);
+              q1 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.y, kLog2eChunk, o)), q1);
+              q2 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.z, kLog2eChunk, o)), q2);
+              q3 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.w, kLog2eChunk, o)), q3);
+            }
+          }
+          acc += fminf(__builtin_amdgcn_exp2f(p.x * kLog2eChunk), q0) +
+                 fminf(__builtin_amdgcn_exp2f(p.y * kLog2eChunk), q1) +
+                 fminf(__builtin_amdgcn_exp2f(p.z * kLog2eChunk), q2) +
+                 fminf(__builtin_amdgcn_exp2f(p.w * kLog2eChunk), q3);
+        }
+        if (res) {
+          // The contract's integer weights. The branch rows are read again here (L2 hits, and
+          // only in the workgroups at a first rejection) so that the rows loaded above need not
+          // stay live; each id's mixture is the binary64 sum over ascending z.
+          uint64_t P[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) P[e] = quant40(detexp32(pe[e]));
+          if (!bonus) {
+            double Q[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 1
+            for (int z = 0; z < R; ++z) {
+              const float4 xz = *reinterpret_cast<const float4*>(trow + z * V + v);
+              const float xe[4] = {xz.x, xz.y, xz.z, xz.w};
+              const double wz = s_wz[z];
+              const float oz = s_offx[z][tt];
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                Q[e] = __dadd_rn(Q[e], __dmul_rn(wz, static_cast<double>(detexp32(__fadd_rn(xe[e], oz)))));
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const uint64_t Qi = quant40d(Q[e]);
+              sr += P[e] > Qi ? P[e] - Qi : 0;
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) sp += P[e];
+        }
+      }
+      if (res) {  // workgroup-uniform: every lane of the half-wave takes part
+#pragma unroll
+        for (int o = 16; o > 0; o >>= 1) {
+          sp += __shfl_xor(sp, o);
+          sr += __shfl_xor(sr, o);
+        }
+        if ((tid & 31) == 0 && tt < nt) {
+          __hip_atomic_store(a.p_tiles + b * k_.nT + t0 + tt, sp, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+          if (!bonus)
+            __hip_atomic_store(a.res_tiles + b * k_.nT + t0 + tt, sr, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
+  }
+  if (!bonus) {
+    acc = wave_sum_f32(acc);
+    if ((tid & 63) == 0) red[tid >> 6] = acc;
+    __syncthreads();
+    if (tid == 0)
+      __hip_atomic_store(a.beta_part + (b * k_.K + k) * nchunk + c,
+                         (red[0] + red[1]) + (red[2] + red[3]), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // Arrival. The partials above are device-coherent stores (written through the XCD's L2); each
+  // wave waits until its own have completed before the count is taken, so a workgroup that
+  // sees the final count sees every partial of the block once it has dropped its cached lines
+  // (one acquire in the last workgroup, instead of an L2 write-back in every workgroup).
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0)
+    s_last = __hip_atomic_fetch_add(a.arrive + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+             static_cast<uint32_t>(rows) * nchunk - 1u;
+  __syncthreads();
+  if (!s_last) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  finalize_block(a, b, nchunk);
+}
+
 }  // namespace
 
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
@@ -511,6 +682,22 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const bool want_beta = a.beta || a.exp_len;
+  if (want_beta && a.arrive && (a.blk.V & 3) == 0) {
+    // One launch: stream, residual tile sums at the first rejection, finalisation.
+    const int rows = static_cast<int>(a.blk.K) + (!a.trajectory && a.Kp == a.blk.K + 1 ? 1 : 0);
+    const int64_t nwg = static_cast<int64_t>(rows) * B * nchunk;
+    if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
+    const dim3 grid(static_cast<unsigned>(nwg));
+    switch (a.blk.R) {
+      case 1: hipLaunchKernelGGL(verify_stream_kernel<1>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
+      case 2: hipLaunchKernelGGL(verify_stream_kernel<2>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
+      case 4: hipLaunchKernelGGL(verify_stream_kernel<4>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
+      case 8: hipLaunchKernelGGL(verify_stream_kernel<8>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
+      case 16: hipLaunchKernelGGL(verify_stream_kernel<16>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
+      default: hipLaunchKernelGGL(verify_stream_kernel<0>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
+    }
+    return hipGetLastError();
+  }
   if (want_beta && !a.trajectory) {
     if (npos + B > 0x7fffffff) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(B + npos), nchunk);
