@@ -156,14 +156,14 @@ __global__ __launch_bounds__(256) void greedy_ptiles_kernel(GreedyArgs a) {
         const int v = 4 * sub + 32 * i;
         if (v0 + v < V) {
           const float4 p4 = *reinterpret_cast<const float4*>(prow + v);
-          sp += quant40(detexp32(p4.x)) + quant40(detexp32(p4.y)) + quant40(detexp32(p4.z)) +
-                quant40(detexp32(p4.w));
+          sp += quant_detexp32(p4.x) + quant_detexp32(p4.y) + quant_detexp32(p4.z) +
+                quant_detexp32(p4.w);
         }
       }
     } else {
       for (int i = 0; i < 16; ++i) {
         const int v = sub + 8 * i;
-        if (v0 + v < V) sp += quant40(detexp32(prow[v]));
+        if (v0 + v < V) sp += quant_detexp32(prow[v]);
       }
     }
   }
@@ -193,7 +193,7 @@ __global__ __launch_bounds__(256) void greedy_finalize_kernel(GreedyArgs a) {
   const float* prow = a.logp + (b * a.Kp + ks) * V;
   const uint32_t r = draw(k_.seed, kResidual, static_cast<uint32_t>(ks),
                           static_cast<uint64_t>(k_.seq_offset + b), k_.step);
-  auto p_int = [&](int64_t v) { return quant40(detexp32(prow[v])); };
+  auto p_int = [&](int64_t v) { return quant_detexp32(prow[v]); };
   int tok = -1;
   if (residual) {
     if (tid == 0) {

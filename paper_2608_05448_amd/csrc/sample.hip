@@ -6,7 +6,9 @@
 //                  (four 16-byte loads) and the tile's exact integer mass
 //                  sum_v floor(q(v) 2^40) goes to the workspace;
 //   sample_select  one 256-thread workgroup per position: inverse CDF over the tile sums, then a
-//                  scan of the selected tile.
+//                  scan of the selected tile (the category is read back from z_out).
+// The integer masses are quant_detexp32 values (the contract's quant40(detexp32(.)) without its
+// branches), summed exactly in binary64: ~30 VALU instructions per vocabulary id.
 // Built with floating-point contraction off: every probability that decides a draw follows
 // the determinism contract exactly.
 #include <hip/hip_runtime.h>
@@ -36,7 +38,8 @@ __global__ __launch_bounds__(256) void sample_tiles_kernel(SampleArgs a) {
   if (blockIdx.y == 0 && k == 0 && threadIdx.x == 0) a.z_out[b] = z;
   const int sub = threadIdx.x & 7;                     // lane within the tile's group of 8
   const int t = blockIdx.y * kTilesPerChunk + (threadIdx.x >> 3);
-  uint64_t s = 0;
+  // The tile's integer mass, summed exactly in binary64 (at most 128 terms below 2^41).
+  double s = 0.0;
   if (z >= 0 && t < k_.nT) {
     const int64_t m = (b * k_.K + k) * k_.R + z;
     const float off = __fsub_rn(k_.lmass[m * k_.nT + t], k_.lse[m]);
@@ -48,22 +51,22 @@ __global__ __launch_bounds__(256) void sample_tiles_kernel(SampleArgs a) {
         const int v = 4 * sub + 32 * i;
         if (v0 + v < k_.V) {
           const float4 x = *reinterpret_cast<const float4*>(row + v);
-          s += quant40(detexp32(__fadd_rn(x.x, off))) + quant40(detexp32(__fadd_rn(x.y, off))) +
-               quant40(detexp32(__fadd_rn(x.z, off))) + quant40(detexp32(__fadd_rn(x.w, off)));
+          s += (quant_detexp32_d(__fadd_rn(x.x, off)) + quant_detexp32_d(__fadd_rn(x.y, off))) +
+               (quant_detexp32_d(__fadd_rn(x.z, off)) + quant_detexp32_d(__fadd_rn(x.w, off)));
         }
       }
     } else {
 #pragma unroll 4
       for (int i = 0; i < 16; ++i) {
         const int v = sub + 8 * i;
-        if (v0 + v < k_.V) s += quant40(detexp32(__fadd_rn(row[v], off)));
+        if (v0 + v < k_.V) s += quant_detexp32_d(__fadd_rn(row[v], off));
       }
     }
   }
   s += __shfl_xor(s, 1);
   s += __shfl_xor(s, 2);
   s += __shfl_xor(s, 4);
-  if (sub == 0 && t < k_.nT) a.tilesum[pos * k_.nT + t] = s;
+  if (sub == 0 && t < k_.nT) a.tilesum[pos * k_.nT + t] = static_cast<uint64_t>(s);
 }
 
 __global__ __launch_bounds__(256) void sample_select_kernel(SampleArgs a) {
@@ -72,7 +75,7 @@ __global__ __launch_bounds__(256) void sample_select_kernel(SampleArgs a) {
   const int64_t pos = blockIdx.x;
   const int64_t b = pos / k_.K;
   const int64_t k = pos % k_.K;
-  const int z = draw_category(k_, b);
+  const int z = a.z_out[b];  // the block's category, written by sample_tiles_kernel
   int x = -1;
   if (z >= 0) {
     const int64_t m = (b * k_.K + k) * k_.R + z;
@@ -83,7 +86,7 @@ __global__ __launch_bounds__(256) void sample_select_kernel(SampleArgs a) {
                             static_cast<uint64_t>(k_.seq_offset + b), k_.step);
     x = select_by_tiles_block(
         a.tilesum + pos * k_.nT, k_.nT, k_.V, r,
-        [&](int64_t v) { return quant40(detexp32(__fadd_rn(row[v], __fsub_rn(lm[v / kTile], lse)))); },
+        [&](int64_t v) { return quant_detexp32(__fadd_rn(row[v], __fsub_rn(lm[v / kTile], lse))); },
         lds);
   }
   if (threadIdx.x == 0) a.x_out[b * k_.K + k] = x;

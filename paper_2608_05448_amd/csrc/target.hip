@@ -249,7 +249,7 @@ __device__ void finish_small(const FilterArgs& a, float* out, uint64_t* cand, in
   const float m = __shfl(sv, 0);
   int nkeep = nk;
   if (a.top_p < 1.0f) {
-    const uint64_t P = lane < nk ? quant40(detexp32(__fsub_rn(sv, m))) : 0;
+    const uint64_t P = lane < nk ? quant_detexp32(__fsub_rn(sv, m)) : 0;
     const uint64_t incl = wave_incl_scan_u64(P);
     const uint64_t z = __shfl(incl, 63);
     uint64_t tp = static_cast<uint64_t>(ceil(__dmul_rn(static_cast<double>(a.top_p),
@@ -335,7 +335,7 @@ __device__ void finish_candidates(const FilterArgs& a, float* out, uint64_t* can
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int i = 4 * tid + j;
-      P[j] = i < nk ? quant40(detexp32(__fsub_rn(key_value(key_at(i)), m))) : 0;
+      P[j] = i < nk ? quant_detexp32(__fsub_rn(key_value(key_at(i)), m)) : 0;
       loc += P[j];
     }
     const uint64_t incl = wave_incl_scan_u64(loc);
@@ -561,7 +561,7 @@ __device__ void filter_general(const FilterArgs& a, const float* in, float* out,
   uint64_t n_tie = ~0ull;
   if (a.top_p < 1.0f) {
     auto mass = [&](float sv, uint32_t k) -> uint64_t {
-      return k >= tk ? quant40(detexp32(__fsub_rn(sv, m))) : 0;
+      return k >= tk ? quant_detexp32(__fsub_rn(sv, m)) : 0;
     };
     uint32_t prefix = 0, pmask = 0;
     uint64_t need = 0, tie_mass = 0;
@@ -690,7 +690,7 @@ __device__ bool filter_nucleus(const FilterArgs& a, const float* in, float* out,
   };
   auto mass_bin = [&](float sv, uint64_t* P) {
     const float d = __fsub_rn(sv, m);
-    *P = quant40(detexp32(d));
+    *P = quant_detexp32(d);
     return min(kNucBins - 1, static_cast<int>(__fmul_rn(-d, kNucScale)));
   };
   // 2. integer mass per bin
@@ -763,7 +763,7 @@ __device__ bool filter_nucleus(const FilterArgs& a, const float* in, float* out,
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int i = 4 * tid + j;
-    P4[j] = i < n ? quant40(detexp32(__fsub_rn(key_value(static_cast<uint32_t>(cand[i] >> 32)), m))) : 0;
+    P4[j] = i < n ? quant_detexp32(__fsub_rn(key_value(static_cast<uint32_t>(cand[i] >> 32)), m)) : 0;
     l4 += P4[j];
   }
   const uint64_t inc4 = wave_incl_scan_u64(l4);

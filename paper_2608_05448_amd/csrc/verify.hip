@@ -270,7 +270,7 @@ struct ResidualWeight {
   int64_t V;
   int nT, R;
   const double* w;     // posterior at the position (R values)
-  __device__ uint64_t p_int(int64_t v) const { return quant40(detexp32(prow[v])); }
+  __device__ uint64_t p_int(int64_t v) const { return quant_detexp32(prow[v]); }
   __device__ uint64_t q_int(int64_t v) const {
     double Q = 0.0;
     for (int z = 0; z < R; ++z) {
@@ -318,7 +318,7 @@ __device__ __forceinline__ void residual_body(const VerifyArgs& a, int64_t b, in
       }
     }
     auto weights = [&](int v, float pv, const float* tv, int tstride, uint64_t& P, uint64_t& Rw) {
-      P = quant40(detexp32(pv));
+      P = quant_detexp32(pv);
       Rw = 0;
       if (!residual) return;
       double Q = 0.0;
@@ -604,7 +604,7 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
           // stay live; each id's mixture is the binary64 sum over ascending z.
           uint64_t P[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) P[e] = quant40(detexp32(pe[e]));
+          for (int e = 0; e < 4; ++e) P[e] = quant_detexp32(pe[e]);
           if (!bonus) {
             double Q[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll 1
