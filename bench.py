@@ -2,12 +2,15 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen3_8b]
                     [--temperature T] [--mode soft|greedy|rows] [--no-cpu-baseline]
-                    [--copy-calibration BYTES]
+                    [--no-extras] [--copy-calibration BYTES]
 
 One step is one pass of the whole hot path over one batch of synthetic inputs already resident
 in HBM: dbl_head_logprobs (bf16 head GEMM + per-tile log-softmax), dbl_sample_block (category
 and token draw) and dbl_verify_block (posterior, accept test, residual/bonus draw, acceptance
-masses, AL_b and E). The Philox step counter advances every step. Prints one JSON line.
+masses, AL_b and E). The Philox step counter advances every step. Prints one JSON line; for the
+Qwen3-8B workload it also carries the same step at the other target temperatures
+(`temperature_sweep`) and the Qwen3-4B and stress workloads' steps (`other_workloads`), unless
+--no-extras.
 With --mode greedy the step is the greedy-branch variant: the head also returns each row's
 argmax, then dbl_sample_greedy and dbl_verify_greedy.
 With --mode rows the line instead times the other entry points at the workload's shape (branch
@@ -19,7 +22,8 @@ head, dbl_expected_len and dbl_acceptance_objective.
 The metric is verified block positions per second, B*K / step time. The roofline entry is for
 the dominant kernel, the head GEMM: 2*M*d*V flops per launch over its average launch time,
 measured with HIP events on the stream the library launches on, against MI355X's dense bf16
-peak. The CPU baseline times the oracle (binary64 NumPy) on a bounded sample of the same
+peak; `roofline.observed` adds the clock and MFMA busy fraction rocprofv3 measured on the same
+head source (profiles/head_bf16_qwen3_8b_clock.json, written by --write-clock). The CPU baseline times the oracle (binary64 NumPy) on a bounded sample of the same
 workload on this machine's host cores.
 """
 from __future__ import annotations
@@ -39,6 +43,9 @@ METRIC = "verified block positions/sec at Qwen3-8B head shape; head-GEMM MFMA % 
 PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "head_bf16_qwen3_8b_traffic.json")
+CLOCK_FILE = os.path.join(ROOT, "profiles", "head_bf16_qwen3_8b_clock.json")
+N_SIMDS = 1024                   # MI355X: 256 CUs x 4 SIMDs
+N_XCDS = 8
 HEAD_SOURCE = os.path.join(ROOT, "paper_2608_05448_amd", "csrc", "head.hip")
 
 
@@ -58,6 +65,53 @@ def _traffic(workload: str):
     if rec.get("head_source_sha256_16") != _head_source_hash() or rec.get("workload") != workload:
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def _clock(workload: str):
+    """Observed clock and MFMA busy of the head kernel from the committed rocprofv3 record, or
+    None when it is missing or was taken on a different head kernel source."""
+    try:
+        with open(CLOCK_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("head_source_sha256_16") != _head_source_hash() or rec.get("workload") != workload:
+        return None
+    return rec
+
+
+def _write_clock(pmc_dir: str, workload: str):
+    """Head clock and MFMA busy from one rocprofv3 run with --pmc GRBM_GUI_ACTIVE
+    SQ_VALU_MFMA_BUSY_CYCLES and --kernel-trace: per head dispatch, GRBM_GUI_ACTIVE / 8 XCDs is
+    the kernel's cycles, (end - start) its duration, and SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x
+    cycles) the MFMA pipes' busy fraction. The first dispatch (warm-up) is left out."""
+    import csv
+    import glob
+    counters, spans = {}, {}
+    for path in glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if "head_bf16" in row["Kernel_Name"]:
+                    d = counters.setdefault(row["Dispatch_Id"], {})
+                    d[row["Counter_Name"]] = d.get(row["Counter_Name"], 0.0) + float(row["Counter_Value"])
+    for path in glob.glob(os.path.join(pmc_dir, "**", "*kernel_trace.csv"), recursive=True):
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if "head_bf16" in row["Kernel_Name"]:
+                    spans[row["Dispatch_Id"]] = (int(row["End_Timestamp"]) - int(row["Start_Timestamp"]))
+    ids = sorted((i for i in counters if i in spans), key=int)[1:]
+    if not ids:
+        raise SystemExit(f"no head dispatches with both counters and a trace under {pmc_dir}")
+    cyc = sum(counters[i]["GRBM_GUI_ACTIVE"] / N_XCDS for i in ids) / len(ids)
+    ns = sum(spans[i] for i in ids) / len(ids)
+    busy = sum(counters[i]["SQ_VALU_MFMA_BUSY_CYCLES"] for i in ids) / len(ids)
+    rec = {"workload": workload, "head_source_sha256_16": _head_source_hash(),
+           "dispatches": len(ids), "head_us": ns / 1e3, "cycles": cyc,
+           "clock_ghz": cyc / ns, "mfma_busy_cycles": busy,
+           "mfma_busy": busy / (N_SIMDS * cyc)}
+    with open(CLOCK_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
 
 
 def _cpu_baseline(wl, h, w, ell, logp, budget_s: float, mode: str = "soft"):
@@ -383,8 +437,13 @@ def main(argv=None):
     ap.add_argument("--temperature", type=float, default=None)
     ap.add_argument("--mode", choices=("soft", "greedy", "rows"), default="soft")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the temperature sweep and the other step workloads")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", type=int, default=0)
+    ap.add_argument("--write-clock", metavar="PMC_DIR",
+                    help="turn a rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES "
+                         "--kernel-trace run into the committed head clock record (no GPU work)")
     ap.add_argument("--write-traffic", nargs=5, metavar=("HEAD_FETCH_DIR", "HEAD_WRITE_DIR",
                                                          "COPY_FETCH_DIR", "COPY_WRITE_DIR",
                                                          "COPY_BYTES"),
@@ -392,6 +451,9 @@ def main(argv=None):
                          "per-launch traffic record (no GPU work)")
     args = ap.parse_args(argv)
 
+    if args.write_clock:
+        _write_clock(args.write_clock, args.workload)
+        return 0
     if args.write_traffic:
         hf, hw, cf, cw, nb = args.write_traffic
         _write_traffic(hf, hw, cf, cw, int(nb), args.workload)
@@ -429,11 +491,112 @@ def main(argv=None):
         print(json.dumps(_objective_chunks(wl, dev, args.steps, args.warmup)), flush=True)
         return 0
 
-    # Inputs resident in HBM before timing.
-    h = synth.make_h(wl, dev)
-    w = synth.make_w(wl, dev)
-    ell = synth.make_ell(wl, dev)
-    logp = synth.make_logp(wl, rows=wl.K + 1, device=dev)
+    head = _step_run(wl, dev, args.mode, args.steps, args.warmup)
+    B, K, R, d, V = wl.B, wl.K, wl.R, wl.d, wl.V
+    step_ms = head["ms_per_step"]
+    M = B * K * R
+    head_ms = head["kernels_ms"]["head"]
+    head_tflops = 2.0 * M * d * V / (head_ms * 1e-3) / 1e12
+    traffic = _traffic(args.workload)
+    roofline = {"bound": "mfma", "achieved": head_tflops, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": head_tflops / PEAK_BF16_TFLOPS, "traffic": traffic,
+                "kernel": "dbl_head_logprobs (head GEMM + per-tile log-softmax, LSE)",
+                "flop_per_launch": 2.0 * M * d * V}
+    clock = _clock(args.workload)
+    if clock is not None:
+        # The 2.5 PFLOP/s peak assumes 2.4 GHz; under this load the clock is lower. All of these
+        # come from the profiled run (counters on), whose head time is its own; the clock this
+        # run's head implies follows from the same cycle count over this run's time.
+        peak_at_clock = PEAK_BF16_TFLOPS * clock["clock_ghz"] / 2.4
+        prof_tflops = 2.0 * M * d * V / (clock["head_us"] * 1e-6) / 1e12
+        roofline["observed"] = {"clock_ghz": clock["clock_ghz"],
+                                "mfma_busy": clock["mfma_busy"],
+                                "head_ms_profiled": clock["head_us"] / 1e3,
+                                "peak_at_clock_tflops": peak_at_clock,
+                                "frac_of_peak_at_clock": prof_tflops / peak_at_clock,
+                                "clock_ghz_implied_here": clock["cycles"] / (head_ms * 1e6),
+                                "source": os.path.relpath(CLOCK_FILE, ROOT)}
+    out = {
+        "metric": METRIC,
+        "value": head["value"],
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "K": K, "R": R, "d": d, "V": V,
+                   "global_batch": B, "positions_per_step": B * K,
+                   "target_temperature": wl.temperature, "z_temp": wl.z_temp,
+                   "mode": args.mode, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "kernels_ms": head["kernels_ms"],
+        "step_ms_p10_p50_p90": head["step_ms_p10_p50_p90"],
+        "hbm": head["hbm"],
+        "quality": head["quality"],
+        "wall_s_timed": head["wall_s_timed"],
+    }
+    if not args.no_extras and args.mode == "soft" and args.workload == "qwen3_8b":
+        # The same step at the other target temperatures of the workload, and the step of the
+        # Qwen3-4B and stress workloads (each with fewer timed steps); the headline is above.
+        n = max(5, args.steps // 2)
+        out["temperature_sweep"] = {}
+        for T in synth.QWEN3_8B_TEMPERATURES:
+            if T == wl.temperature:
+                continue
+            r = _step_run(wl.replace(temperature=T), dev, "soft", n, 3, with_inputs=True)
+            out["temperature_sweep"][str(T)] = {k: r[k] for k in ("value", "ms_per_step",
+                                                                  "kernels_ms", "quality")}
+        out["other_workloads"] = {}
+        for name in ("qwen3_4b", "stress"):
+            ow = synth.WORKLOADS[name]
+            r = _step_run(ow, dev, "soft", n, 3)
+            r.pop("wall_s_timed", None)
+            ohead = r["kernels_ms"]["head"]
+            r["config"] = {"B": ow.B, "K": ow.K, "R": ow.R, "d": ow.d, "V": ow.V,
+                           "target_temperature": ow.temperature}
+            r["head_frac_of_bf16_peak"] = (2.0 * ow.B * ow.K * ow.R * ow.d * ow.V /
+                                           (ohead * 1e-3) / 1e12 / PEAK_BF16_TFLOPS)
+            out["other_workloads"][name] = r
+    if not args.no_cpu_baseline:
+        h, w, ell, logp = _inputs(wl, dev)
+        out["cpu_baseline"] = _cpu_baseline(wl, h, w, ell, logp, args.cpu_budget, args.mode)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+_INPUT_CACHE = {}
+
+
+def _inputs(wl, dev):
+    """Synthetic inputs of a workload, resident in HBM (kept for the process: the temperature
+    sweep reuses the branch states and weights and regenerates only the target)."""
+    import synth
+    key = (wl.name, wl.temperature)
+    if key not in _INPUT_CACHE:
+        base = next((v for k, v in _INPUT_CACHE.items() if k[0] == wl.name), None)
+        if base is None:
+            if any(k[0] != wl.name for k in _INPUT_CACHE):
+                _INPUT_CACHE.clear()
+            h, w, ell = synth.make_h(wl, dev), synth.make_w(wl, dev), synth.make_ell(wl, dev)
+        else:
+            h, w, ell = base[:3]
+        _INPUT_CACHE[key] = (h, w, ell, synth.make_logp(wl, rows=wl.K + 1, device=dev))
+    return _INPUT_CACHE[key]
+
+
+def _step_run(wl, dev, mode, steps, warmup, with_inputs=False):
+    """Time `steps` steps (after `warmup`) of head + draw + verification on the workload, with
+    HIP events on the library's stream; inputs resident in HBM before timing."""
+    import torch
+
+    from paper_2608_05448_amd import dblast as D
+
+    h, w, ell, logp = _inputs(wl, dev)
     B, K, R, d, V = wl.B, wl.K, wl.R, wl.d, wl.V
     nT = D.ntiles(V)
     tls = torch.empty((B, K, R, V), dtype=torch.float32, device=dev)
@@ -450,7 +613,7 @@ def main(argv=None):
                        device=dev)
     ws_v = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_VERIFY, B, K, R, d, V), dtype=torch.uint8,
                        device=dev)
-    greedy = args.mode == "greedy"
+    greedy = mode == "greedy"
     am = torch.empty((B, K, R), dtype=torch.int32, device=dev)
     ws_h = torch.empty(D.dbl_workspace_bytes(D.DBL_OP_HEAD, B, K, R, d, V), dtype=torch.uint8,
                        device=dev)
@@ -484,72 +647,43 @@ def main(argv=None):
         if ev is not None:
             ev[3].record(stream)
 
-    for t in range(args.warmup):
+    for t in range(warmup):
         step(t)
     torch.cuda.synchronize(dev)
-
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    acc_sum = 0.0
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
     torch.cuda.synchronize(dev)
     t_wall = time.perf_counter()
-    for i in range(args.steps):
-        step(args.warmup + i, events[i])
+    for i in range(steps):
+        step(warmup + i, events[i])
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t_wall
 
-    head_ms = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
-    sample_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps
-    verify_ms = sum(e[2].elapsed_time(e[3]) for e in events) / args.steps
-    step_ms = events[0][0].elapsed_time(events[-1][3]) / args.steps
+    head_ms = sum(e[0].elapsed_time(e[1]) for e in events) / steps
+    sample_ms = sum(e[1].elapsed_time(e[2]) for e in events) / steps
+    verify_ms = sum(e[2].elapsed_time(e[3]) for e in events) / steps
+    step_ms = events[0][0].elapsed_time(events[-1][3]) / steps
     per_step = sorted(e[0].elapsed_time(e[3]) for e in events)
     pct = {q: per_step[min(len(per_step) - 1, int(q / 100 * len(per_step)))] for q in (10, 50, 90)}
-    acc_sum = float(vout["n_accept"].float().mean().item())
-    exp_len = float(vout["exp_len"].float().mean().item())
-
-    M = B * K * R
-    head_flop = 2.0 * M * d * V
-    head_tflops = head_flop / (head_ms * 1e-3) / 1e12
     # Algorithmic bytes: soft verify streams R branch rows + the target row per position; the
     # soft draw one branch row per position. Greedy verify streams one target row per block
     # (the first rejected position or the bonus row); the greedy draw reads no vocabulary row.
     verify_bytes = B * V * 4.0 if greedy else B * K * (R + 1) * V * 4.0
     sample_bytes = 0.0 if greedy else B * K * V * 4.0
-    traffic = _traffic(args.workload)
-
-    out = {
-        "metric": METRIC,
+    return {
         "value": B * K / (step_ms * 1e-3),
-        "unit": "positions/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": step_ms,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": args.workload, "B": B, "K": K, "R": R, "d": d, "V": V,
-                   "global_batch": B, "positions_per_step": B * K,
-                   "target_temperature": wl.temperature, "z_temp": wl.z_temp,
-                   "mode": args.mode, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "achieved": head_tflops, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": head_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": traffic,
-                     "kernel": "dbl_head_logprobs (head GEMM + per-tile log-softmax, LSE)"},
         "kernels_ms": {"head": head_ms, "sample": sample_ms, "verify": verify_ms},
         "step_ms_p10_p50_p90": [pct[10], pct[50], pct[90]],
         "hbm": {"verify_GBps": verify_bytes / (verify_ms * 1e-3) / 1e9,
                 "verify_frac": verify_bytes / (verify_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                "verify_bytes": verify_bytes,
                 "sample_GBps": sample_bytes / (sample_ms * 1e-3) / 1e9,
                 "sample_frac": sample_bytes / (sample_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
-        "quality": {"mean_n_accept": acc_sum, "mean_exp_len": exp_len},
+        "quality": {"mean_n_accept": float(vout["n_accept"].float().mean().item()),
+                    "mean_exp_len": float(vout["exp_len"].float().mean().item()),
+                    "mean_al_expected": float(vout["al_expected"].float().mean().item())},
         "wall_s_timed": wall,
     }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = _cpu_baseline(wl, h, w, ell, logp, args.cpu_budget, args.mode)
-    print(json.dumps(out), flush=True)
-    return 0
 
 
 if __name__ == "__main__":

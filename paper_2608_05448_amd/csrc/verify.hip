@@ -15,12 +15,12 @@
 //             the bonus row when every position was accepted.
 //   finalize  one 256-thread workgroup per block: acceptance masses,
 //             E = sum_i prod_{j<=i} beta_j, and the residual/bonus inverse-CDF draw.
-//   stream    (V % 4 == 0, masses requested: the usual case) beta, residual and finalize in one
-//             launch after the chain: the residual's tile sums come from the stream's own loads
-//             at the first rejected position, and the last of a block's workgroups to finish
-//             finalises it.
-// The same kernels serve the expected-length reduction along a given trajectory (no accept
-// test, no residual). Built with floating-point contraction off (determinism contract).
+//   stream    (verification with V % 4 == 0 and masses requested: the usual case) beta,
+//             residual and finalize in one launch after the chain: the residual's tile sums come
+//             from the stream's own loads at the first rejected position, and the last of a
+//             block's workgroups to finish finalises it.
+// The expected-length reduction along a given trajectory runs chain, beta and finalize (no
+// accept test, no residual). Built with floating-point contraction off (determinism contract).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -519,10 +519,14 @@ __global__ __launch_bounds__(256) void finalize_kernel(VerifyArgs a, int nchunk)
 // it. Counting replaces the separate finalize launch; nothing waits on another workgroup.
 constexpr float kLog2eChunk = 1.4426950408889634f;
 
-// Eight waves per SIMD (64 VGPRs): the binary64 residual arithmetic, which only the workgroups
-// at a first rejection run, would otherwise set the register budget of every workgroup.
+// Eight waves per SIMD (64 VGPRs) up to eight categories: the binary64 residual arithmetic, which
+// only the workgroups at a first rejection run, would otherwise set the register budget of every
+// workgroup. Sixteen categories keep their 16 row loads in flight in 80 VGPRs (six waves).
 template <int RT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8, 8)))
+constexpr int stream_waves() { return RT > 8 ? 6 : 8; }
+
+template <int RT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(stream_waves<RT>(), 8)))
 void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
   const BlockArgs& k_ = a.blk;
   const int64_t B = k_.B;
@@ -568,11 +572,10 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
       uint64_t sp = 0, sr = 0;
       if (v < ve) {
         const float4 p = *reinterpret_cast<const float4*>(prow + v);
-        const float pe[4] = {p.x, p.y, p.z, p.w};
-        float4 x[RT > 0 ? RT : 1];
-        if (!bonus) {
+        if (!bonus && !res) {
           float q0 = 0.0f, q1 = 0.0f, q2 = 0.0f, q3 = 0.0f;
           if constexpr (RT > 0) {
+            float4 x[RT];
 #pragma unroll
             for (int z = 0; z < RT; ++z) x[z] = *reinterpret_cast<const float4*>(trow + z * V + v);
 #pragma unroll
@@ -597,34 +600,41 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
                  fminf(__builtin_amdgcn_exp2f(p.y * kLog2eChunk), q1) +
                  fminf(__builtin_amdgcn_exp2f(p.z * kLog2eChunk), q2) +
                  fminf(__builtin_amdgcn_exp2f(p.w * kLog2eChunk), q3);
-        }
-        if (res) {
-          // The contract's integer weights. The branch rows are read again here (L2 hits, and
-          // only in the workgroups at a first rejection) so that the rows loaded above need not
-          // stay live; each id's mixture is the binary64 sum over ascending z.
-          uint64_t P[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) P[e] = quant_detexp32(pe[e]);
-          if (!bonus) {
-            double Q[4] = {0.0, 0.0, 0.0, 0.0};
+        } else if (!bonus) {
+          // The first rejected position: one pass over each branch row feeds both the binary32
+          // mixture of the acceptance mass (same operations in the same order as above) and the
+          // contract's binary64 mixture of the residual weights, so no row is read twice (with
+          // every wave of the chip streaming, a second read would miss the L2).
+          const float pe[4] = {p.x, p.y, p.z, p.w};
+          float q[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+          double Q[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll 1
-            for (int z = 0; z < R; ++z) {
-              const float4 xz = *reinterpret_cast<const float4*>(trow + z * V + v);
-              const float xe[4] = {xz.x, xz.y, xz.z, xz.w};
-              const double wz = s_wz[z];
-              const float oz = s_offx[z][tt];
-#pragma unroll
-              for (int e = 0; e < 4; ++e)
-                Q[e] = __dadd_rn(Q[e], __dmul_rn(wz, static_cast<double>(detexp32(__fadd_rn(xe[e], oz)))));
-            }
+          for (int z = 0; z < R; ++z) {
+            const float4 xz = *reinterpret_cast<const float4*>(trow + z * V + v);
+            const float xe[4] = {xz.x, xz.y, xz.z, xz.w};
+            const float oz = s_offx[z][tt];
+            const float o = oz * kLog2eChunk, w = s_w[z];
+            const double wz = s_wz[z];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const uint64_t Qi = quant40d(Q[e]);
-              sr += P[e] > Qi ? P[e] - Qi : 0;
+              q[e] = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xe[e], kLog2eChunk, o)), q[e]);
+              Q[e] = __dadd_rn(Q[e], __dmul_rn(wz, static_cast<double>(detexp32(__fadd_rn(xe[e], oz)))));
             }
           }
+          acc += fminf(__builtin_amdgcn_exp2f(p.x * kLog2eChunk), q[0]) +
+                 fminf(__builtin_amdgcn_exp2f(p.y * kLog2eChunk), q[1]) +
+                 fminf(__builtin_amdgcn_exp2f(p.z * kLog2eChunk), q[2]) +
+                 fminf(__builtin_amdgcn_exp2f(p.w * kLog2eChunk), q[3]);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) sp += P[e];
+          for (int e = 0; e < 4; ++e) {
+            const uint64_t P = quant_detexp32(pe[e]);
+            const uint64_t Qi = quant40d(Q[e]);
+            sr += P > Qi ? P - Qi : 0;
+            sp += P;
+          }
+        } else {  // the bonus row after full acceptance: P only
+          sp = (quant_detexp32(p.x) + quant_detexp32(p.y)) +
+               (quant_detexp32(p.z) + quant_detexp32(p.w));
         }
       }
       if (res) {  // workgroup-uniform: every lane of the half-wave takes part
@@ -682,8 +692,10 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const bool want_beta = a.beta || a.exp_len;
-  if (want_beta && a.arrive && (a.blk.V & 3) == 0) {
-    // One launch: stream, residual tile sums at the first rejection, finalisation.
+  if (want_beta && a.arrive && (a.blk.V & 3) == 0 && !a.trajectory) {
+    // One launch: stream, residual tile sums at the first rejection, finalisation. Trajectory
+    // mode keeps the two launches below: its stream kernel has no residual arithmetic to carry,
+    // and at R = 16 it measured 3.48 ms against 3.78 ms fused per 128-block chunk.
     const int rows = static_cast<int>(a.blk.K) + (!a.trajectory && a.Kp == a.blk.K + 1 ? 1 : 0);
     const int64_t nwg = static_cast<int64_t>(rows) * B * nchunk;
     if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
