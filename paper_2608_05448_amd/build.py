@@ -76,5 +76,24 @@ def build(verbose: bool = False, jobs: int = 4, extra_flags=(), out: str = LIB,
     return out
 
 
+TEST_HELPER_SRC = os.path.join(ROOT, "tests", "native", "contract_check.hip")
+TEST_HELPER_LIB = os.path.join(ROOT, "tests", "native", "libcontract_check.so")
+
+
+def build_test_helper(verbose: bool = False) -> str:
+    """Compile the GPU test helper (an exhaustive check of the contract's quantised exponential,
+    loaded only by the tests) with the library's flags and contraction off."""
+    cc = hipcc()
+    tmp = TEST_HELPER_LIB + ".tmp"
+    cmd = [cc, *COMMON, "-ffp-contract=off", "-shared", TEST_HELPER_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {TEST_HELPER_SRC}:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, TEST_HELPER_LIB)
+    return TEST_HELPER_LIB
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
