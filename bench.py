@@ -497,12 +497,12 @@ def main(argv=None):
     M = B * K * R
     head_ms = head["kernels_ms"]["head"]
     head_tflops = 2.0 * M * d * V / (head_ms * 1e-3) / 1e12
-    traffic = _traffic(args.workload)
+    traffic = _traffic(args.workload) if args.mode == "soft" else None
     roofline = {"bound": "mfma", "achieved": head_tflops, "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": head_tflops / PEAK_BF16_TFLOPS, "traffic": traffic,
                 "kernel": "dbl_head_logprobs (head GEMM + per-tile log-softmax, LSE)",
                 "flop_per_launch": 2.0 * M * d * V}
-    clock = _clock(args.workload)
+    clock = _clock(args.workload) if args.mode == "soft" else None  # taken on the soft head
     if clock is not None:
         # The 2.5 PFLOP/s peak assumes 2.4 GHz; under this load the clock is lower. All of these
         # come from the profiled run (counters on), whose head time is its own; the clock this
