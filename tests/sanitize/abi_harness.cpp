@@ -58,7 +58,7 @@ hipError_t launch_read_probe(const void*, int64_t, float*, int64_t, hipStream_t)
 
 int main(int argc, char** argv) {
   if (argc > 1 && strcmp(argv[1], "--plant-overflow") == 0) {
-    // Shows that the sanitizer is live in this build: one read past a heap array.
+    // Shows that the sanitizer is active: one read past a heap array.
     volatile int* v = new int[4];
     const int x = v[argc + 2];
     delete[] v;
