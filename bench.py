@@ -151,10 +151,55 @@ def _cpu_baseline(wl, h, w, ell, logp, budget_s: float, mode: str = "soft"):
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     cores = len(os.sched_getaffinity(0))
     return {"value": done * K / el, "unit": "positions/s", "cores": min(threads, cores),
-            "kind": "oracle",
+            "kind": "oracle", "host": _host_cpu(),
             "sample": f"{done} of {wl.B} blocks ({done * K} positions): binary64 head, "
                       f"{'greedy-branch ' if mode == 'greedy' else ''}block draw and "
                       f"verification, {el:.1f} s on the host"}
+
+
+def _host_cpu() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _cpu_baseline_objective(wl, h, w, ell, xs, logp, budget_s: float):
+    """The oracle on whole blocks of one chunk of the objective workload (binary64 head, the
+    expected length along the trajectory and the objective forward) until the time budget."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import head as OH
+    from oracle import mixture as MX
+    from oracle import objective as OB
+
+    ww = w.float().cpu().numpy()
+    hh = h.float().cpu().numpy()
+    ee = ell.cpu().numpy()
+    xx = xs.cpu().numpy()
+    lp = logp.cpu().numpy()
+    K, R, d, V = wl.K, wl.R, wl.d, wl.V
+    t0 = time.perf_counter()
+    done = 0
+    for b in range(len(xx)):
+        tls, lm, ls = OH.head_factored(hh[b].reshape(K * R, d), ww, v_chunk=8192)
+        lq = OH.flat_logq(tls, lm, ls).reshape(1, K, R, V)
+        MX.expected_len_blocks(lq, ee[b:b + 1], wl.z_temp, xx[b:b + 1], lp[b:b + 1])
+        OB.acceptance_objective(lq, ee[b:b + 1], wl.z_temp, xx[b:b + 1], lp[b:b + 1], tau=0.1)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": done * K / el, "unit": "positions/s",
+            "cores": min(threads, len(os.sched_getaffinity(0))), "kind": "oracle",
+            "host": _host_cpu(),
+            "sample": f"{done} of {wl.B} blocks ({done * K} positions): binary64 head, expected "
+                      f"length along the trajectory and objective forward, {el:.1f} s on the host"}
 
 
 def _pmc_mean(csv_dir: str, counter: str, name_re: str) -> float:
@@ -343,7 +388,8 @@ def _rows(wl, dev, steps: int, warmup: int, cpu: bool = True):
                        "target_rows": B * (K + 1)}}
 
 
-def _objective_chunks(wl, dev, steps: int, warmup: int, chunk: int = 128):
+def _objective_chunks(wl, dev, steps: int, warmup: int, chunk: int = 128, cpu: bool = True,
+                      cpu_budget: float = 12.0):
     """The training-objective workload (2048 blocks, R = 16): one step runs every chunk of
     `chunk` blocks through dbl_head_logprobs, dbl_expected_len (β and E along the target
     trajectory) and dbl_acceptance_objective, with all chunks' inputs resident in HBM."""
@@ -425,7 +471,10 @@ def _objective_chunks(wl, dev, steps: int, warmup: int, chunk: int = 128):
                     "expected_len_frac": el_bytes / (el_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
             "quality": {"mean_exp_len_last_chunk": float(e.mean().item()),
                         "mean_J_last_chunk": float(obj["J"].mean().item())},
-            "wall_s_timed": wall}
+            "wall_s_timed": wall,
+            **({"cpu_baseline": _cpu_baseline_objective(wl, chunks[0][0], w, chunks[0][3],
+                                                        chunks[0][2], chunks[0][1], cpu_budget)}
+               if cpu else {})}
 
 
 def main(argv=None):
@@ -488,7 +537,9 @@ def main(argv=None):
               flush=True)
         return 0
     if wl.name == "objective":
-        print(json.dumps(_objective_chunks(wl, dev, args.steps, args.warmup)), flush=True)
+        print(json.dumps(_objective_chunks(wl, dev, args.steps, args.warmup,
+                                           cpu=not args.no_cpu_baseline,
+                                           cpu_budget=args.cpu_budget)), flush=True)
         return 0
 
     head = _step_run(wl, dev, args.mode, args.steps, args.warmup)
