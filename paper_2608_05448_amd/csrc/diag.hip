@@ -1,11 +1,13 @@
 // Streaming-read probe: the plain read rate that bounds the bandwidth-bound kernels (the
 // acceptance-mass stream, the draw's tile sums, the target transform). Every 16-byte word of
-// a buffer is read once with float4 loads, four in flight per thread; each workgroup writes the
-// sum of what it read, so the loads cannot be dropped.
+// a buffer is read once with 16-byte non-temporal loads (the form those kernels use), four in
+// flight per thread; each workgroup writes the sum of what it read, so the loads cannot be
+// dropped.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "kernels.hpp"
+#include "wave.hpp"
 
 namespace dbl {
 namespace {
@@ -24,7 +26,8 @@ __global__ __launch_bounds__(kProbeThreads) void read_probe_kernel(const float4*
 #pragma unroll
     for (int u = 0; u < kProbeUnroll; ++u) {
       const int64_t j = i + u * kProbeThreads;
-      v[u] = j < n4 ? x[j] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      v[u] = j < n4 ? load_stream4(reinterpret_cast<const float*>(x + j))
+                    : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     }
 #pragma unroll
     for (int u = 0; u < kProbeUnroll; ++u) acc += (v[u].x + v[u].y) + (v[u].z + v[u].w);

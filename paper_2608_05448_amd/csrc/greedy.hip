@@ -155,7 +155,7 @@ __global__ __launch_bounds__(256) void greedy_ptiles_kernel(GreedyArgs a) {
       for (int i = 0; i < 4; ++i) {
         const int v = 4 * sub + 32 * i;
         if (v0 + v < V) {
-          const float4 p4 = *reinterpret_cast<const float4*>(prow + v);
+          const float4 p4 = load_stream4(prow + v);
           sp += quant_detexp32(p4.x) + quant_detexp32(p4.y) + quant_detexp32(p4.z) +
                 quant_detexp32(p4.w);
         }

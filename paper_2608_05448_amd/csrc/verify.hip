@@ -210,12 +210,12 @@ __device__ __forceinline__ void beta_body(const VerifyArgs& a, int64_t pos, int 
   if ((V & 3) == 0) {
     for (int64_t v = vb + 4 * threadIdx.x; v < ve; v += 4 * blockDim.x) {
       const int tt = static_cast<int>((v - vb) >> 7);
-      const float4 p = *reinterpret_cast<const float4*>(prow + v);
+      const float4 p = load_stream4(prow + v);
       float4 x[RT > 0 ? RT : 1];
       float q0 = 0.0f, q1 = 0.0f, q2 = 0.0f, q3 = 0.0f;
       if constexpr (RT > 0) {
 #pragma unroll
-        for (int z = 0; z < RT; ++z) x[z] = *reinterpret_cast<const float4*>(trow + z * V + v);
+        for (int z = 0; z < RT; ++z) x[z] = load_stream4(trow + z * V + v);
 #pragma unroll
         for (int z = 0; z < RT; ++z) {
           const float o = s_off[z][tt], w = s_w[z];
@@ -226,7 +226,7 @@ __device__ __forceinline__ void beta_body(const VerifyArgs& a, int64_t pos, int 
         }
       } else {
         for (int z = 0; z < R; ++z) {
-          const float4 xz = *reinterpret_cast<const float4*>(trow + z * V + v);
+          const float4 xz = load_stream4(trow + z * V + v);
           const float o = s_off[z][tt], w = s_w[z];
           q0 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.x, kLog2eF, o)), q0);
           q1 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.y, kLog2eF, o)), q1);
@@ -344,14 +344,14 @@ __device__ __forceinline__ void residual_body(const VerifyArgs& a, int64_t b, in
       for (int i = 0; i < 4; ++i) {
         const int v = 4 * sub + 32 * i;
         if (v0 + v < V) {
-          const float4 p4 = *reinterpret_cast<const float4*>(prow + v);
+          const float4 p4 = load_stream4(prow + v);
           const float pe[4] = {p4.x, p4.y, p4.z, p4.w};
           float4 x4[RT > 0 ? RT : 1];
           if constexpr (RT > 0) {
             if (residual) {
 #pragma unroll
               for (int z = 0; z < RT; ++z)
-                x4[z] = *reinterpret_cast<const float4*>(trow + z * V + v);
+                x4[z] = load_stream4(trow + z * V + v);
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -571,13 +571,13 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
       const int tt = (4 * tid + 1024 * i) >> 7;  // the 32 threads of a half-wave share a tile
       uint64_t sp = 0, sr = 0;
       if (v < ve) {
-        const float4 p = *reinterpret_cast<const float4*>(prow + v);
+        const float4 p = load_stream4(prow + v);
         if (!bonus && !res) {
           float q0 = 0.0f, q1 = 0.0f, q2 = 0.0f, q3 = 0.0f;
           if constexpr (RT > 0) {
             float4 x[RT];
 #pragma unroll
-            for (int z = 0; z < RT; ++z) x[z] = *reinterpret_cast<const float4*>(trow + z * V + v);
+            for (int z = 0; z < RT; ++z) x[z] = load_stream4(trow + z * V + v);
 #pragma unroll
             for (int z = 0; z < RT; ++z) {
               const float o = s_offx[z][tt] * kLog2eChunk, w = s_w[z];
@@ -588,7 +588,7 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
             }
           } else {
             for (int z = 0; z < R; ++z) {
-              const float4 xz = *reinterpret_cast<const float4*>(trow + z * V + v);
+              const float4 xz = load_stream4(trow + z * V + v);
               const float o = s_offx[z][tt] * kLog2eChunk, w = s_w[z];
               q0 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.x, kLog2eChunk, o)), q0);
               q1 = fmaf(w, __builtin_amdgcn_exp2f(fmaf(xz.y, kLog2eChunk, o)), q1);
@@ -610,7 +610,7 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
           double Q[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll 1
           for (int z = 0; z < R; ++z) {
-            const float4 xz = *reinterpret_cast<const float4*>(trow + z * V + v);
+            const float4 xz = load_stream4(trow + z * V + v);
             const float xe[4] = {xz.x, xz.y, xz.z, xz.w};
             const float oz = s_offx[z][tt];
             const float o = oz * kLog2eChunk, w = s_w[z];

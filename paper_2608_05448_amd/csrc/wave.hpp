@@ -11,6 +11,23 @@ namespace dbl {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// 16-byte load of data that a launch reads exactly once (the rows of the acceptance-mass stream,
+// a target row), with the non-temporal hint so that it does not displace cached lines: a linear
+// 1.4 GB read measured 7.0-7.2 TB/s this way against 6.2-6.5 TB/s with plain loads, the
+// verification stream 6-9% faster and the expected-length stream 11% faster.
+#ifndef DBL_NT_LOADS
+#define DBL_NT_LOADS 1
+#endif
+typedef float stream_f32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 load_stream4(const float* p) {
+#if DBL_NT_LOADS
+  const stream_f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const stream_f32x4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+#else
+  return *reinterpret_cast<const float4*>(p);
+#endif
+}
+
 // Value of lane l (wave-uniform l) in every lane: v_readlane on each 32-bit half, a few cycles
 // instead of an LDS-crossbar shuffle.
 __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
