@@ -382,6 +382,25 @@ def _rows(wl, dev, steps: int, warmup: int, cpu: bool = True):
     rows["reference_read"] = hbm(ms, buf.numel() * 4.0)
     ms = timed(lambda: dst.copy_(buf))
     rows["reference_copy"] = hbm(ms, buf.numel() * 8.0)
+    del buf, dst
+    # Reference for the head: the vendor library's plain bf16 GEMM of the same shape (hipBLASLt
+    # through torch's linear: logits = h w^T, bf16 output, no log-softmax), against the library
+    # head (GEMM + fused per-tile log-softmax, fp32 output, LSE).
+    hh = synth.make_h(wl, dev).reshape(B * K * R, d)
+    ww = synth.make_w(wl, dev)
+    logits = torch.empty((B * K * R, V), dtype=torch.bfloat16, device=dev)
+    ms = timed(lambda: torch.matmul(hh, ww.t(), out=logits))
+    flop = 2.0 * B * K * R * d * V
+    rows["reference_gemm"] = {"ms": ms, "bound": "mfma", "tflops": flop / (ms * 1e-3) / 1e12,
+                              "frac": flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                              "what": "torch.matmul (hipBLASLt), bf16 in and out, no epilogue"}
+    del logits
+    tls = torch.empty((B, K, R, V), dtype=torch.float32, device=dev)
+    lmass = torch.empty((B, K, R, D.ntiles(V)), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, K, R), dtype=torch.float32, device=dev)
+    ms = timed(lambda: D.dbl_head_logprobs(hh.view(B, K, R, d), ww, tls, lmass, lse))
+    rows["head_logprobs"] = {"ms": ms, "bound": "mfma", "tflops": flop / (ms * 1e-3) / 1e12,
+                             "frac": flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
     return {"metric": "per-call time of the entry points outside the step", "rows": rows,
             "steps": steps, "warmup": warmup, "data": "synthetic",
             "config": {"workload": wl.name, "B": B, "K": K, "R": R, "d": d, "V": V,
