@@ -6,9 +6,10 @@
 // 16 logits of one branch row. The per-tile (128 ids) max and sum of exponentials therefore
 // reduce in registers plus one cross-half exchange, and the tile-normalised log-probs are
 // stored straight from the accumulators: logits never reach memory. Operand feeds, by hidden
-// size: d % 64 == 0, 64-deep stages staged through registers (the main path; the branch
-// expander uses the same kernel with narrower tiles); d % 32 == 0, 32-deep stages copied global
-// -> LDS directly; otherwise a register-staged kernel with padded LDS rows.
+// size: d % 64 == 0, the 8-wave ping-pong kernel with 64-deep stages copied global -> LDS
+// directly (the main path); d % 32 == 0, 32-deep stages copied global -> LDS by four waves;
+// otherwise a register-staged kernel with padded LDS rows. The branch expander runs a
+// register-staged kernel with 64-deep stages and 128 x 256 tiles.
 //
 // fp32 path: a plain fp32 kernel for fp32 inputs (small problems).
 #include <hip/hip_runtime.h>
@@ -806,8 +807,9 @@ __global__ __launch_bounds__(C::kThreads, C::kWgPerCu) void head_bf16_dma_kernel
 
 
 // ---------------------------------------------------------------------------------------
-// Register-staged variant (hidden sizes that are a multiple of 64): 64-deep stages, so every
-// 128-byte row segment of a stage is one request, and a lead of two stages for every load.
+// Register-staged kernel (the expander's GEMM, hidden sizes that are a multiple of 64; it was
+// the head's main path before the ping-pong kernel): 64-deep stages, so every 128-byte row
+// segment of a stage is one request, and a lead of two stages for every load.
 // The LDS holds two stages (128 KB); two more stages are in flight in registers (16 16-byte
 // loads per thread per stage): during stage kt the threads write stage kt + 1 from registers
 // to the LDS slot stage kt - 1 has left and refill those registers with stage kt + 3. The main
@@ -845,8 +847,7 @@ struct RsCfg {
   static_assert(NF <= 2 * NSLOT, "at most two fragment loads per MFMA pair");
   static_assert(2 * (TILEA + TILEB) <= 160 * 1024, "two stages in LDS");
 };
-using RsHead = RsCfg<256, 256, 2, 2>;   // the head: 256 x 256 tiles
-using RsNarrow = RsCfg<128, 256, 1, 4>; // few branch rows (the expander): 128 x 256 tiles
+using RsNarrow = RsCfg<128, 256, 1, 4>; // few trunk rows (the expander): 128 x 256 tiles
 
 template <class C, int EPI>
 __global__ __launch_bounds__(C::kThreads, 1) void head_bf16_rs_kernel(
@@ -1355,13 +1356,7 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
     const int vec4 = (a.V % 4 == 0) ? 1 : 0;
     const __bf16* h = static_cast<const __bf16*>(a.h);
     const __bf16* w = static_cast<const __bf16*>(a.w);
-#ifndef DBL_HEAD_RS
-#define DBL_HEAD_RS 1
-#endif
-#ifndef DBL_HEAD_PP
-#define DBL_HEAD_PP 1
-#endif
-    if (DBL_HEAD_PP && a.d % PpCfg::BK == 0) {
+    if (a.d % PpCfg::BK == 0) {
       const int dm = static_cast<int>((a.M + PpCfg::BM - 1) / PpCfg::BM);
       const int64_t dwg = ((a.V + PpCfg::BV - 1) / PpCfg::BV) * dm;
       if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
@@ -1378,23 +1373,6 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t stream) {
       else
         hipLaunchKernelGGL(head_bf16_pp_kernel<false>, grid, block, 0, stream, h, w, ea, a.M,
                            a.V, a.d, dm);
-    } else if (DBL_HEAD_RS && a.d % RsHead::BK == 0) {
-      const int dm = static_cast<int>((a.M + RsHead::BM - 1) / RsHead::BM);
-      const int64_t dwg = ((a.V + RsHead::BV - 1) / RsHead::BV) * dm;
-      if (dwg > 0x7fffffff) return hipErrorInvalidConfiguration;
-      const dim3 grid(static_cast<unsigned>(dwg)), block(RsHead::kThreads);
-      EpiArgs ea{};
-      ea.tls = a.tls;
-      ea.lmass = a.lmass;
-      ea.amax = amax;
-      ea.nT = nT;
-      ea.vec4 = vec4;
-      if (amax)
-        hipLaunchKernelGGL((head_bf16_rs_kernel<RsHead, kEpiLogSoftmaxArgmax>), grid, block, 0, stream, h,
-                           w, ea, a.M, a.V, a.d, dm);
-      else
-        hipLaunchKernelGGL((head_bf16_rs_kernel<RsHead, kEpiLogSoftmax>), grid, block, 0, stream, h, w,
-                           ea, a.M, a.V, a.d, dm);
     } else if (a.d % DCfg::BK == 0) {
       const int dm = static_cast<int>((a.M + DCfg::BM - 1) / DCfg::BM);
       const int64_t dwg = ((a.V + DCfg::BV - 1) / DCfg::BV) * dm;
