@@ -1,9 +1,9 @@
 // Block draw from the DBLast latent mixture (Sec. "Dependent Block Drafting and Verification":
 // draw a category from the prior, then every position of the block in parallel from that
 // branch). Two kernels:
-//   sample_tiles   grid (position, chunk of 32 vocabulary tiles), 256 threads: the drawn
-//                  category's row is streamed once; 8 lanes per 128-id tile each quantise 16 ids
-//                  (four 16-byte loads) and the tile's exact integer mass
+//   sample_tiles   grid (position, group of three chunks of 32 vocabulary tiles), 256 threads:
+//                  the drawn category's row is streamed once; 8 lanes per 128-id tile each
+//                  quantise 16 ids (four 16-byte loads) and the tile's exact integer mass
 //                  sum_v floor(q(v) 2^40) goes to the workspace;
 //   sample_select  one 256-thread workgroup per position: inverse CDF over the tile sums, then a
 //                  scan of the selected tile (the category is read back from z_out).
@@ -21,6 +21,11 @@
 namespace dbl {
 namespace {
 
+// Chunks of 32 tiles per workgroup: every workgroup first waits for its wavefront 0's category
+// draw, so three chunks share that wait (18% faster than one at the Qwen3-8B shape, 15% at the
+// stress shape; 2, 4, 6 and 8 measured between).
+constexpr int kChunksPerGroup = 3;
+
 __global__ __launch_bounds__(256) void sample_tiles_kernel(SampleArgs a) {
   const BlockArgs& k_ = a.blk;
   const int64_t pos = blockIdx.x;
@@ -37,38 +42,41 @@ __global__ __launch_bounds__(256) void sample_tiles_kernel(SampleArgs a) {
   const int z = s_z;
   if (blockIdx.y == 0 && k == 0 && threadIdx.x == 0) a.z_out[b] = z;
   const int sub = threadIdx.x & 7;                     // lane within the tile's group of 8
-  const int t = blockIdx.y * kTilesPerChunk + (threadIdx.x >> 3);
-  // The tile's integer mass, summed exactly in binary64 (at most 128 terms below 2^41).
-  double s = 0.0;
-  if (z >= 0 && t < k_.nT) {
-    const int64_t m = (b * k_.K + k) * k_.R + z;
-    const float off = __fsub_rn(k_.lmass[m * k_.nT + t], k_.lse[m]);
-    const int64_t v0 = static_cast<int64_t>(t) * kTile;
-    const float* row = k_.tls + m * k_.V + v0;
-    if ((k_.V & 3) == 0) {
+#pragma unroll 1
+  for (int cc = 0; cc < kChunksPerGroup; ++cc) {
+    const int t = (blockIdx.y * kChunksPerGroup + cc) * kTilesPerChunk + (threadIdx.x >> 3);
+    // The tile's integer mass, summed exactly in binary64 (at most 128 terms below 2^41).
+    double s = 0.0;
+    if (z >= 0 && t < k_.nT) {
+      const int64_t m = (b * k_.K + k) * k_.R + z;
+      const float off = __fsub_rn(k_.lmass[m * k_.nT + t], k_.lse[m]);
+      const int64_t v0 = static_cast<int64_t>(t) * kTile;
+      const float* row = k_.tls + m * k_.V + v0;
+      if ((k_.V & 3) == 0) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int v = 4 * sub + 32 * i;
-        if (v0 + v < k_.V) {
-          // Plain loads: this kernel is bound by VALU issue, and the non-temporal form measured
-          // 5% slower here.
-          const float4 x = *reinterpret_cast<const float4*>(row + v);
-          s += (quant_detexp32_d(__fadd_rn(x.x, off)) + quant_detexp32_d(__fadd_rn(x.y, off))) +
-               (quant_detexp32_d(__fadd_rn(x.z, off)) + quant_detexp32_d(__fadd_rn(x.w, off)));
+        for (int i = 0; i < 4; ++i) {
+          const int v = 4 * sub + 32 * i;
+          if (v0 + v < k_.V) {
+            // Plain loads: this kernel is bound by VALU issue, and the non-temporal form
+            // measured 5% slower here.
+            const float4 x = *reinterpret_cast<const float4*>(row + v);
+            s += (quant_detexp32_d(__fadd_rn(x.x, off)) + quant_detexp32_d(__fadd_rn(x.y, off))) +
+                 (quant_detexp32_d(__fadd_rn(x.z, off)) + quant_detexp32_d(__fadd_rn(x.w, off)));
+          }
+        }
+      } else {
+#pragma unroll 4
+        for (int i = 0; i < 16; ++i) {
+          const int v = sub + 8 * i;
+          if (v0 + v < k_.V) s += quant_detexp32_d(__fadd_rn(row[v], off));
         }
       }
-    } else {
-#pragma unroll 4
-      for (int i = 0; i < 16; ++i) {
-        const int v = sub + 8 * i;
-        if (v0 + v < k_.V) s += quant_detexp32_d(__fadd_rn(row[v], off));
-      }
     }
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    if (sub == 0 && t < k_.nT) a.tilesum[pos * k_.nT + t] = static_cast<uint64_t>(s);
   }
-  s += __shfl_xor(s, 1);
-  s += __shfl_xor(s, 2);
-  s += __shfl_xor(s, 4);
-  if (sub == 0 && t < k_.nT) a.tilesum[pos * k_.nT + t] = static_cast<uint64_t>(s);
 }
 
 __global__ __launch_bounds__(256) void sample_select_kernel(SampleArgs a) {
@@ -100,7 +108,8 @@ hipError_t launch_sample(const SampleArgs& a, hipStream_t stream) {
   const int64_t npos = a.blk.B * a.blk.K;
   const int nchunk = n_chunks(a.blk.nT);
   if (npos > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(sample_tiles_kernel, dim3(static_cast<unsigned>(npos), nchunk), dim3(256),
+  const int ngroups = (nchunk + kChunksPerGroup - 1) / kChunksPerGroup;
+  hipLaunchKernelGGL(sample_tiles_kernel, dim3(static_cast<unsigned>(npos), ngroups), dim3(256),
                      0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
