@@ -8,7 +8,8 @@
 //   greedy_sample    one wavefront per block: category draw, branch copy;
 //   greedy_chain     one wavefront per block, lane = category: consistent set, pi~ (log-domain
 //                    normalisation of the prior restricted to C_k), q at the drafted token, the
-//                    accept chain, A_k / AL_b, beta_k over the support tokens and E;
+//                    accept chain, A_k / AL_b, beta_k over the support tokens and E; for staged
+//                    blocks (the usual case) a parallel form handles every position at once;
 //   greedy_ptiles    grid (block, vocabulary chunk): integer tile sums of the target row at the
 //                    first rejected position (or the bonus row);
 //   greedy_finalize  one 256-thread workgroup per block: the residual tile sums are the target
@@ -136,6 +137,139 @@ __global__ __launch_bounds__(64) void greedy_chain_kernel(GreedyArgs a) {
   }
 }
 
+// Parallel form of greedy_chain_kernel for staged blocks (K <= kGreedyStageK and
+// K * R <= kGreedyStageKR), one 256-thread workgroup per block. The consistent set at position k
+// depends only on the drafted prefix, so every position is handled at once: lane z of the
+// wavefront holding position k reads whether branch z matched every drafted token before k (a
+// bit mask per branch), normalises pi~ with the same wavefront operations, and forms q at the
+// drafted token and beta_k over the support tokens; one thread then takes E in position order,
+// and wavefront 0 runs the integer accept chain. Bit-identical to greedy_chain_kernel.
+__global__ __launch_bounds__(256) void greedy_chain_parallel_kernel(GreedyArgs a) {
+  const BlockArgs& k_ = a.blk;
+  const int64_t b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid >> 6;
+  constexpr int kWaves = 4;
+  const int R = static_cast<int>(k_.R);
+  const int K = static_cast<int>(k_.K);
+  const int KR = K * R;
+  const int64_t V = k_.V;
+  const uint64_t seq = static_cast<uint64_t>(k_.seq_offset + b);
+  __shared__ int32_t s_x[kGreedyStageK];
+  __shared__ float s_px[kGreedyStageK];
+  __shared__ int32_t s_t[kGreedyStageKR];
+  __shared__ float s_pt[kGreedyStageKR];
+  __shared__ double s_L0[kMaxR];
+  __shared__ uint64_t s_mask[kMaxR];  // bit k: branch z's token is the drafted token at k
+  __shared__ double s_w[kWaves][64];
+  __shared__ double s_Q[kGreedyStageK];
+  __shared__ double s_P[kGreedyStageK];
+  __shared__ double s_beta[kGreedyStageK];
+  for (int k = tid; k < K; k += blockDim.x) s_x[k] = a.x[b * k_.K + k];
+  for (int i = tid; i < KR; i += blockDim.x) s_t[i] = a.xhat[b * k_.K * k_.R + i];
+  if (wave == 0) {
+    const double l0 = prior_log_weight(k_.prior + b * k_.R, R, k_.z_temp);
+    if (lane < R) s_L0[lane] = l0;
+  }
+  __syncthreads();
+  for (int k = tid; k < K; k += blockDim.x) {
+    const int32_t xk = s_x[k];
+    s_px[k] = in_vocab(xk, V) ? a.logp[(b * a.Kp + k) * V + xk] : 0.0f;
+  }
+  for (int i = tid; i < KR; i += blockDim.x) {
+    const int32_t t = s_t[i];
+    s_pt[i] = in_vocab(t, V) ? a.logp[(b * a.Kp + i / R) * V + t] : 0.0f;
+  }
+  if (tid < R) {
+    uint64_t m = 0;
+    for (int k = 0; k < K; ++k)
+      if (s_t[k * R + tid] == s_x[k]) m |= uint64_t{1} << k;
+    s_mask[tid] = m;
+  }
+  __syncthreads();
+  const bool want_beta = a.beta || a.exp_len;
+  for (int k = wave; k < K; k += kWaves) {
+    const uint64_t before = (uint64_t{1} << k) - 1;  // positions 0 .. k - 1 (k < 64)
+    const bool consistent = lane < R && (s_mask[lane] & before) == before;
+    const double w = normalize_weight(consistent ? s_L0[lane] : -INFINITY, R);
+    const int64_t row = (b * k_.K + k) * k_.R;
+    if (lane < R) a.wpost[row + lane] = w;
+    const int32_t xk = s_x[k];
+    const int32_t t = lane < R ? s_t[k * R + lane] : -1;
+    const bool match = lane < R && t == xk;
+    if (!a.trajectory) {
+      double Q = 0.0;
+      for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, lane_f64(match ? w : 0.0, z));
+      const double P = in_vocab(xk, V) ? static_cast<double>(detexp32(s_px[k])) : 0.0;
+      if (lane == 0) {
+        s_Q[k] = Q;
+        s_P[k] = P;
+      }
+    }
+    if (want_beta) {
+      s_w[wave][lane] = lane < R ? w : 0.0;
+      // Wavefront-private LDS: the writes above precede these reads in the wavefront's queue.
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // Lane z represents its token if it is the lowest category with weight on that token;
+      // q(token) is the ascending-z sum of the weights of every category proposing it.
+      double contrib = 0.0;
+      if (lane < R && w > 0.0 && in_vocab(t, V)) {
+        bool first = true;
+        double q = 0.0;
+        for (int z = 0; z < R; ++z) {
+          if (s_w[wave][z] > 0.0 && s_t[k * R + z] == t) {
+            if (z < lane) first = false;
+            q = __dadd_rn(q, s_w[wave][z]);
+          }
+        }
+        if (first) contrib = fmin(exp(static_cast<double>(s_pt[k * R + lane])), q);
+      }
+      const double beta_k = wave_sum_f64(contrib);
+      if (lane == 0) {
+        s_beta[k] = beta_k;
+        if (a.beta) a.beta[b * k_.K + k] = static_cast<float>(beta_k);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+  }
+  __syncthreads();
+  if (tid == 0 && a.exp_len) {
+    double prodB = 1.0, E = 0.0;
+    for (int k = 0; k < K; ++k) {
+      prodB *= s_beta[k];
+      E += prodB;
+    }
+    a.exp_len[b] = static_cast<float>(E);
+  }
+  if (a.trajectory || wave != 0) return;
+  // Wavefront 0: every position's accept test at once (the draws do not depend on earlier
+  // outcomes); n_accept is the first rejection, and the running product of the A_k is taken in
+  // position order by every lane alike.
+  const int k = lane;
+  bool rej = false;
+  double A = 0.0;
+  if (k < K) {
+    const double Q = s_Q[k], P = s_P[k];
+    A = Q > 0.0 ? fmin(1.0, P / Q) : (P > 0.0 ? 1.0 : 0.0);
+    const uint32_t r = draw(k_.seed, kAccept, static_cast<uint32_t>(k), seq, k_.step);
+    rej = !accept_int(r, quant40d(Q), quant40d(P));
+  }
+  const uint64_t rejm = __ballot(rej);
+  const int n_acc = rejm ? __ffsll(static_cast<unsigned long long>(rejm)) - 1 : K;
+  double prodA = 1.0, al = 0.0;
+  for (int j = 0; j < K; ++j) {
+    prodA = __dmul_rn(prodA, lane_f64(A, j));
+    al = __dadd_rn(al, prodA);
+  }
+  if (lane == 0) {
+    a.n_accept[b] = n_acc;
+    if (a.al) a.al[b] = static_cast<float>(al);
+  }
+}
+
 // Integer tile sums floor(detexp32(logp) 2^40) of the target row at position n_accept[b] (the
 // first rejected position, or the bonus row K); 8 lanes per 128-id tile.
 __global__ __launch_bounds__(256) void greedy_ptiles_kernel(GreedyArgs a) {
@@ -183,6 +317,9 @@ __global__ __launch_bounds__(256) void greedy_finalize_kernel(GreedyArgs a) {
   __shared__ int32_t s_tok[kMaxR];
   __shared__ uint64_t s_q[kMaxR];
   __shared__ double s_qd[kMaxR];
+  __shared__ double s_wz[kMaxR];
+  __shared__ int32_t s_tz[kMaxR];
+  __shared__ uint64_t s_p[kMaxR];
   __shared__ int s_n;
   const int ks = a.n_accept[b];
   const bool residual = ks < k_.K;
@@ -196,15 +333,21 @@ __global__ __launch_bounds__(256) void greedy_finalize_kernel(GreedyArgs a) {
   auto p_int = [&](int64_t v) { return quant_detexp32(prow[v]); };
   int tok = -1;
   if (residual) {
+    // The posterior and branch tokens at ks, gathered in parallel.
+    const int64_t row = (b * k_.K + ks) * k_.R;
+    if (tid < k_.R) {
+      s_wz[tid] = a.wpost[row + tid];
+      s_tz[tid] = a.xhat[row + tid];
+    }
+    __syncthreads();
     if (tid == 0) {
       // Support of q at ks: distinct branch tokens of the categories with weight, with
       // q(token) summed over ascending z and quantised.
       int n = 0;
-      const int64_t row = (b * k_.K + ks) * k_.R;
       for (int z = 0; z < k_.R; ++z) {
-        const double w = a.wpost[row + z];
+        const double w = s_wz[z];
         if (!(w > 0.0)) continue;
-        const int32_t t = a.xhat[row + z];
+        const int32_t t = s_tz[z];
         int j = 0;
         while (j < n && s_tok[j] != t) ++j;
         if (j == n) {
@@ -219,10 +362,12 @@ __global__ __launch_bounds__(256) void greedy_finalize_kernel(GreedyArgs a) {
     for (int t = tid; t < nT; t += blockDim.x)
       a.res_tiles[b * nT + t] = a.p_tiles[b * nT + t];
     __syncthreads();
+    if (tid < s_n && in_vocab(s_tok[tid], V)) s_p[tid] = p_int(s_tok[tid]);
+    __syncthreads();
     if (tid == 0) {
       for (int j = 0; j < s_n; ++j) {
         if (!in_vocab(s_tok[j], V)) continue;
-        const uint64_t P = p_int(s_tok[j]);
+        const uint64_t P = s_p[j];
         a.res_tiles[b * nT + s_tok[j] / kTile] -= P < s_q[j] ? P : s_q[j];
       }
     }
@@ -255,7 +400,11 @@ hipError_t launch_sample_greedy(const GreedyArgs& a, hipStream_t stream) {
 hipError_t launch_verify_greedy(const GreedyArgs& a, hipStream_t stream) {
   const int64_t B = a.blk.B;
   if (B > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(greedy_chain_kernel, dim3(static_cast<unsigned>(B)), dim3(64), 0, stream, a);
+  if (a.blk.K <= kGreedyStageK && a.blk.K * a.blk.R <= kGreedyStageKR)
+    hipLaunchKernelGGL(greedy_chain_parallel_kernel, dim3(static_cast<unsigned>(B)), dim3(256), 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL(greedy_chain_kernel, dim3(static_cast<unsigned>(B)), dim3(64), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.trajectory) return e;
   hipLaunchKernelGGL(greedy_ptiles_kernel, dim3(static_cast<unsigned>(B), n_chunks(a.blk.nT)),
