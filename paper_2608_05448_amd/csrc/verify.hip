@@ -24,6 +24,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "contract.hpp"
 #include "kernels.hpp"
 #include "wave.hpp"
@@ -80,8 +82,10 @@ __global__ __launch_bounds__(64) void chain_kernel(VerifyArgs a) {
 // per block). The posterior at position k depends only on the drafted prefix, not on the
 // accept decisions, so every position is handled at once: thread (k, z) folds its own prefix
 // L_{k,z} = (((L_{0,z} + lq_{0,z}) + lq_{1,z}) + ...) + lq_{k-1,z} in the same order as the
-// sequential walk, wavefront k normalises it and forms q_k(x_k | x_<k), and one thread then
-// runs the integer accept chain over k. Bit-identical to chain_kernel.
+// sequential walk, a segment of lanes per position normalises it and forms q_k(x_k | x_<k)
+// (eight positions per wavefront at R <= 8: the normalisation's serial steps were 56% of the
+// kernel with one position per wavefront), and one wavefront then runs the integer accept chain
+// over k. Bit-identical to chain_kernel.
 constexpr int kChainMaxKR = 2048;
 constexpr int kChainMaxK = 256;
 
@@ -129,18 +133,34 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
     s_L[i] = L;
   }
   __syncthreads();
+  // 64 / G positions per wavefront at a time, one segment of G lanes each (lane z = category).
   const int nwaves = blockDim.x >> 6;
-  for (int k = wave; k < K; k += nwaves) {
-    const double L = lane < R ? s_L[k * R + lane] : -INFINITY;
-    const double w = normalize_weight(L, R);
-    if (lane < R) a.wpost[(b * k_.K + k) * k_.R + lane] = w;
-    if (!a.trajectory) {
-      const double y = lane < R ? static_cast<double>(detexp32(s_lq[k * R + lane])) : 0.0;
-      double Q = 0.0;
-      for (int z = 0; z < R; ++z) Q = __dadd_rn(Q, __dmul_rn(lane_f64(w, z), lane_f64(y, z)));
-      if (lane == 0) s_Q[k] = Q;
+  auto weights = [&](auto g_c) {
+    constexpr int G = decltype(g_c)::value, P = 64 / G;
+    const int seg = lane / G, z = lane % G;
+    for (int k0 = wave * P; k0 < K; k0 += nwaves * P) {
+      const int k = k0 + seg;
+      const bool own = k < K && z < R;
+      const double L = own ? s_L[k * R + z] : -INFINITY;
+      const double w = normalize_weight_seg<G>(L, R);
+      if (own) a.wpost[(b * k_.K + k) * k_.R + z] = w;
+      if (!a.trajectory) {
+        const double y = own ? static_cast<double>(detexp32(s_lq[k * R + z])) : 0.0;
+        double Q = 0.0;
+        for (int zz = 0; zz < R; ++zz)
+          Q = __dadd_rn(Q, __dmul_rn(__shfl(w, seg * G + zz), __shfl(y, seg * G + zz)));
+        if (k < K && z == 0) s_Q[k] = Q;
+      }
     }
-  }
+  };
+  if (R <= 8)
+    weights(std::integral_constant<int, 8>{});
+  else if (R <= 16)
+    weights(std::integral_constant<int, 16>{});
+  else if (R <= 32)
+    weights(std::integral_constant<int, 32>{});
+  else
+    weights(std::integral_constant<int, 64>{});
   if (a.trajectory) return;
   __syncthreads();
   // Wavefront 0: 64 positions' accept tests at a time (the draws do not depend on earlier

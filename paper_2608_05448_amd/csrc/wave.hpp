@@ -105,6 +105,21 @@ __device__ __forceinline__ double normalize_weight(double L, int R) {
   return e / S;
 }
 
+// normalize_weight for several positions per wavefront: lanes in segments of G (a power of two,
+// R <= G <= 64), lane z of a segment holding category z's log weight. Each segment gets exactly
+// what normalize_weight gives a wavefront holding the same values (same operations, same order).
+template <int G>
+__device__ __forceinline__ double normalize_weight_seg(double L, int R) {
+  const int base = lane_id() & ~(G - 1);
+  double mx = __shfl(L, base);
+  for (int z = 1; z < R; ++z) mx = fmax(mx, __shfl(L, base + z));
+  if (!(mx > -INFINITY)) return 0.0;
+  const double e = dexp64(__dsub_rn(L, mx));
+  double S = 0.0;
+  for (int z = 0; z < R; ++z) S = __dadd_rn(S, __shfl(e, base + z));
+  return e / S;
+}
+
 // The category z ~ q_{Z_T} of block b by inverse CDF on floor(w_z 2^40); all lanes agree.
 __device__ __forceinline__ int draw_category(const BlockArgs& a, int64_t b) {
   const int lane = lane_id();
