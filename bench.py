@@ -1,13 +1,15 @@
 """Throughput of the DBLast head + block draw + verification on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen3_8b]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--settle-ms MS] [--workload qwen3_8b]
                     [--temperature T] [--mode soft|greedy|rows] [--no-cpu-baseline]
                     [--no-extras] [--copy-calibration BYTES]
 
 One step is one pass of the whole hot path over one batch of synthetic inputs already resident
 in HBM: dbl_head_logprobs (bf16 head GEMM + per-tile log-softmax), dbl_sample_block (category
 and token draw) and dbl_verify_block (posterior, accept test, residual/bonus draw, acceptance
-masses, AL_b and E). The Philox step counter advances every step. Prints one JSON line; for the
+masses, AL_b and E). The Philox step counter advances every step. Before the W warm-up steps the
+step runs untimed for --settle-ms of wall time (default 100), since the GPU's clock ramps for
+~40 ms from idle; the line reports it under `settle`. Prints one JSON line; for the
 Qwen3-8B workload it also carries the same step at the other target temperatures
 (`temperature_sweep`) and the Qwen3-4B and stress workloads' steps (`other_workloads`), unless
 --no-extras.
@@ -501,6 +503,9 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle-ms", type=float, default=100.0,
+                    help="untimed steps for at least this much wall time before the warm-up "
+                         "steps, so the clock is at its sustained level (0: none)")
     ap.add_argument("--workload", default="qwen3_8b")
     ap.add_argument("--temperature", type=float, default=None)
     ap.add_argument("--mode", choices=("soft", "greedy", "rows"), default="soft")
@@ -561,7 +566,7 @@ def main(argv=None):
                                            cpu_budget=args.cpu_budget)), flush=True)
         return 0
 
-    head = _step_run(wl, dev, args.mode, args.steps, args.warmup)
+    head = _step_run(wl, dev, args.mode, args.steps, args.warmup, settle_ms=args.settle_ms)
     B, K, R, d, V = wl.B, wl.K, wl.R, wl.d, wl.V
     step_ms = head["ms_per_step"]
     M = B * K * R
@@ -609,6 +614,7 @@ def main(argv=None):
         "hbm": head["hbm"],
         "quality": head["quality"],
         "wall_s_timed": head["wall_s_timed"],
+        "settle": head["settle"],
     }
     if not args.no_extras and args.mode == "soft" and args.workload == "qwen3_8b":
         # The same step at the other target temperatures of the workload, and the step of the
@@ -626,6 +632,7 @@ def main(argv=None):
             ow = synth.WORKLOADS[name]
             r = _step_run(ow, dev, "soft", n, 3)
             r.pop("wall_s_timed", None)
+            r.pop("settle", None)
             ohead = r["kernels_ms"]["head"]
             r["config"] = {"B": ow.B, "K": ow.K, "R": ow.R, "d": ow.d, "V": ow.V,
                            "target_temperature": ow.temperature}
@@ -659,7 +666,7 @@ def _inputs(wl, dev):
     return _INPUT_CACHE[key]
 
 
-def _step_run(wl, dev, mode, steps, warmup, with_inputs=False):
+def _step_run(wl, dev, mode, steps, warmup, with_inputs=False, settle_ms=0.0):
     """Time `steps` steps (after `warmup`) of head + draw + verification on the workload, with
     HIP events on the library's stream; inputs resident in HBM before timing."""
     import torch
@@ -717,6 +724,17 @@ def _step_run(wl, dev, mode, steps, warmup, with_inputs=False):
         if ev is not None:
             ev[3].record(stream)
 
+    # From idle the GPU's clock takes ~40 ms of this load to reach its sustained level (per-step
+    # time 3.7 ms at the first step, 2.55 ms at the sixth, steady from about the seventeenth at
+    # the Qwen3-8B shape), so before the warm-up steps the step runs for at least settle_ms of
+    # wall time; the line reports how many steps that took.
+    settle_steps = 0
+    t_settle = time.perf_counter()
+    while (time.perf_counter() - t_settle) * 1e3 < settle_ms:
+        for _ in range(4):
+            step(settle_steps)
+            settle_steps += 1
+        torch.cuda.synchronize(dev)
     for t in range(warmup):
         step(t)
     torch.cuda.synchronize(dev)
@@ -753,6 +771,7 @@ def _step_run(wl, dev, mode, steps, warmup, with_inputs=False):
                     "mean_exp_len": float(vout["exp_len"].float().mean().item()),
                     "mean_al_expected": float(vout["al_expected"].float().mean().item())},
         "wall_s_timed": wall,
+        "settle": {"ms": settle_ms, "steps": settle_steps},
     }
 
 
