@@ -144,7 +144,9 @@ def _cpu_baseline(wl, h, w, ell, logp, budget_s: float, mode: str = "soft"):
         else:
             tls, lm, ls = OH.head_factored(hh[b].reshape(K * R, d), ww, v_chunk=8192)
             lq = OH.flat_logq(tls, lm, ls).reshape(1, K, R, V)
-            _, x = MX.sample_blocks(lq, ee[b:b + 1], wl.z_temp, wl.philox_seed, 0, seq)
+            _, x = MX.sample_blocks(tls.reshape(1, K, R, V), lm.reshape(1, K, R, -1),
+                                    ls.reshape(1, K, R), ee[b:b + 1], wl.z_temp,
+                                    wl.philox_seed, 0, seq)
             MX.verify_blocks(lq, ee[b:b + 1], wl.z_temp, x, lp[b:b + 1], wl.philox_seed, 0, seq)
         done += 1
         if time.perf_counter() - t0 >= budget_s:

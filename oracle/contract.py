@@ -11,8 +11,10 @@ floating-point probability becomes a discrete decision. This module fixes that r
 that two independent implementations (this one and the HIP kernels) take every discrete
 decision identically:
 
-* every uniform draw is word 0 of Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel Random
-  Numbers: As Easy as 1, 2, 3", SC'11), keyed by the seed and indexed by what it is for;
+* every uniform draw is a word of Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel Random
+  Numbers: As Easy as 1, 2, 3", SC'11), keyed by the seed and indexed by what it is for: word 0,
+  and for the drafted token's second stage (the id within its 128-id tile) word 1 of the same
+  counter;
 * every probability that feeds a decision comes from a deterministic exponential built only
   from separately rounded IEEE add/sub/mul, round-to-nearest-even and exact power-of-two
   scaling (Cody-Waite range reduction followed by a Taylor polynomial in Horner form);
@@ -96,6 +98,13 @@ def draw_u32(seed: int, purpose: int, k: int, seq: int, step: int) -> int:
     """
     seed = int(seed) & 0xFFFFFFFFFFFFFFFF
     return philox4x32_10((k, purpose, seq, step), (seed & MASK32, seed >> 32))[0]
+
+
+def draw_u32_word1(seed: int, purpose: int, k: int, seq: int, step: int) -> int:
+    """Output word 1 of the same Philox block as ``draw_u32`` (the drafted token's id within
+    the tile that word 0 selected)."""
+    seed = int(seed) & 0xFFFFFFFFFFFFFFFF
+    return philox4x32_10((k, purpose, seq, step), (seed & MASK32, seed >> 32))[1]
 
 
 class PhiloxDraws:

@@ -7,6 +7,9 @@ R latent categories z (the paper writes b for the block length and K for the num
 categories). For block b the inputs are
 
 * lq[b, k, z, :]  binary32 log q_k(. | y, z), the branch token log-probabilities;
+* for the draw, the same log-probabilities in the head's two-level form: tls[b, k, z, :]
+  (log-probability within each 128-id tile), lmass[b, k, z, :] (tile log-masses) and
+  lse[b, k, z] (their log-sum-exp), lq = fl32(tls + fl32(lmass - lse));
 * ell[b, :]       binary32 category logits l_z(y);
 * logp[b, k, :]   binary32 target log-probabilities p_k(.) = p(. | y, x_<k); an optional extra
                   row k = K feeds the bonus token.
@@ -17,7 +20,10 @@ What is computed, in the paper's order:
    q_{Z_T}(z) = softmax(l / Z_T); Z_T = 0 selects the highest-prior category (appendix,
    "Greedy-Branch Proposal"), ties going to the lowest index.
 2. Block draw from the mixture of Eq. cp-drafter: first z ~ q_{Z_T}, then every position
-   independently from q_k(. | z).
+   independently from q_k(. | z). The paper leaves open how a token is drawn from q_k(. | z);
+   here it is drawn in two stages that follow the two-level form: first the 128-id tile t
+   with probability exp(lmass_t - lse), then the id v within it with probability exp(tls_v)
+   (their product is q_k(v | z)), each stage an inverse CDF on its quantised weights.
 3. Verification of a drafted block with the prefix-marginalised conditional of
    Eq. dep-conditional, computed through the category posterior of Eq. category-posterior,
        w_{k,z} proportional to q_{Z_T}(z) prod_{j<k} q_j(x_j | z),
@@ -50,12 +56,12 @@ from .contract import (PURPOSE_ACCEPT, PURPOSE_CATEGORY, PURPOSE_RESIDUAL, PURPO
                        accept_int, detexp32, dexp64, icdf, philox4x32_10_np, quant40)
 
 
-def draws(seed: int, purpose: int, k: int, seq, step: int):
-    """Philox word 0 for (purpose, k) and every sequence index in ``seq`` (array)."""
+def draws(seed: int, purpose: int, k: int, seq, step: int, word: int = 0):
+    """Philox word ``word`` (0 or 1) for (purpose, k) and every sequence index in ``seq``."""
     seed = int(seed) & 0xFFFFFFFFFFFFFFFF
     seq = np.asarray(seq, dtype=np.uint64)
     out = philox4x32_10_np(k, purpose, seq, int(step), seed & 0xFFFFFFFF, seed >> 32)
-    return out[0]
+    return out[word]
 
 
 # ----------------------------------------------------------------------------------------
@@ -109,24 +115,48 @@ def _mixture_fp64(w, y):
 # ----------------------------------------------------------------------------------------
 # 2. Block draw
 # ----------------------------------------------------------------------------------------
-def sample_blocks(lq, ell, z_temp, seed, step, seq):
+TILE = 128  # ids per tile of the two-level form
+
+
+def draw_token(tls_row, lmass_row, lse, r_tile: int, r_id: int) -> int:
+    """One token from the two-level form of a branch row: the tile by an inverse CDF on
+    floor(detexp32(fl32(lmass_t - lse)) 2^40) with word r_tile, then the id within it by an
+    inverse CDF on floor(detexp32(tls_v) 2^40) with word r_id. -1 if no tile has quantised
+    mass."""
+    tls_row = np.asarray(tls_row, dtype=np.float32)
+    lmass_row = np.asarray(lmass_row, dtype=np.float32)
+    off = (lmass_row - np.float32(lse)).astype(np.float32)
+    t = icdf(quant40(detexp32(off)), r_tile)
+    if t < 0:
+        return -1
+    ids = tls_row[t * TILE:(t + 1) * TILE]
+    j = icdf(quant40(detexp32(ids)), r_id)
+    return -1 if j < 0 else t * TILE + j
+
+
+def sample_blocks(tls, lmass, lse, ell, z_temp, seed, step, seq):
     """Draw z ~ q_{Z_T} and x_k ~ q_k(. | z) for every block.
 
-    lq [B, K, R, V] float32, ell [B, R] float32, seq [B] global sequence indices.
+    tls [B, K, R, V], lmass [B, K, R, nT], lse [B, K, R] float32 (the two-level form of the
+    branch log-probabilities), ell [B, R] float32, seq [B] global sequence indices.
     Returns z [B] int32 and x [B, K] int32 (-1 marks a row with no quantised mass).
     """
-    lq = np.asarray(lq, dtype=np.float32)
-    B, K, R, V = lq.shape
+    tls = np.asarray(tls, dtype=np.float32)
+    lmass = np.asarray(lmass, dtype=np.float32)
+    lse = np.asarray(lse, dtype=np.float32)
+    B, K, R, V = tls.shape
     seq = np.asarray(seq)
     pi_q = quant40(prior(ell, z_temp))
     r_cat = draws(seed, PURPOSE_CATEGORY, 0, seq, step)
     z = np.array([icdf(pi_q[b], r_cat[b]) for b in range(B)], dtype=np.int32)
     x = np.empty((B, K), dtype=np.int32)
     for k in range(K):
-        r_tok = draws(seed, PURPOSE_TOKEN, k, seq, step)
+        r_tile = draws(seed, PURPOSE_TOKEN, k, seq, step, word=0)
+        r_id = draws(seed, PURPOSE_TOKEN, k, seq, step, word=1)
         for b in range(B):
-            row = quant40(detexp32(lq[b, k, z[b]]))
-            x[b, k] = icdf(row, r_tok[b])
+            zb = z[b]
+            x[b, k] = draw_token(tls[b, k, zb], lmass[b, k, zb], lse[b, k, zb], r_tile[b],
+                                 r_id[b])
     return z, x
 
 

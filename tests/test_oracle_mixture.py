@@ -35,6 +35,13 @@ def _probs(lq):
     return np.exp(np.asarray(lq, dtype=np.float64))
 
 
+def _one_tile(lq):
+    """The two-level form of rows that fit one 128-id tile: tls = lq, lmass = lse = 0."""
+    lq = np.asarray(lq, dtype=np.float32)
+    assert lq.shape[-1] <= MX.TILE
+    return lq, np.zeros(lq.shape[:-1] + (1,), np.float32), np.zeros(lq.shape[:-1], np.float32)
+
+
 # ---------------------------------------------------------------------------------------
 # Prior
 # ---------------------------------------------------------------------------------------
@@ -133,7 +140,7 @@ def test_block_draw_law_is_the_mixture_joint():
     """Two-stage draw (z, then positions in parallel) samples Eq. cp-drafter."""
     K, R, V, N = 2, 2, 3, 8000
     lq, ell, _ = tiny_case(41, N, K, R, V, q_scale=1.5)
-    z, x = MX.sample_blocks(lq, ell, 1.0, seed=5, step=2, seq=np.arange(N))
+    z, x = MX.sample_blocks(*_one_tile(lq), ell, 1.0, seed=5, step=2, seq=np.arange(N))
     pi = MX.prior(ell[:1], 1.0)[0]
     assert _chi2_pvalue(np.bincount(z, minlength=R), pi) > 1e-4
     joint = EN.block_joint(_probs(lq[0]), pi).reshape(-1)
@@ -144,11 +151,84 @@ def test_block_draw_law_is_the_mixture_joint():
 def test_single_category_reduces_to_independent_block_sampling():
     K, V, N = 2, 4, 8000
     lq, ell, _ = tiny_case(43, N, K, 1, V, q_scale=1.5)
-    z, x = MX.sample_blocks(lq, ell, 1.0, seed=9, step=0, seq=np.arange(N))
+    z, x = MX.sample_blocks(*_one_tile(lq), ell, 1.0, seed=9, step=0, seq=np.arange(N))
     assert np.all(z == 0)
     q = _probs(lq[0, :, 0])
     cells = np.bincount(x[:, 0] * V + x[:, 1], minlength=V * V)
     assert _chi2_pvalue(cells, np.outer(q[0], q[1]).reshape(-1)) > 1e-4
+
+
+def _two_level(logits):
+    """Binary32 two-level form of binary64 logits [..., V] (tile log-prob, tile log-mass,
+    log-sum-exp), built here from the definitions of a tile-wise log-softmax."""
+    lg = np.asarray(logits, dtype=np.float64)
+    V = lg.shape[-1]
+    nT = -(-V // MX.TILE)
+    lmass = np.stack([np.log(np.exp(lg[..., t * MX.TILE:(t + 1) * MX.TILE]).sum(-1))
+                      for t in range(nT)], -1)
+    tls = lg - np.repeat(lmass, MX.TILE, axis=-1)[..., :V]
+    lse = np.log(np.exp(lg).sum(-1))
+    return tls.astype(np.float32), lmass.astype(np.float32), lse.astype(np.float32)
+
+
+def _token_law(tls_row, lmass_row, lse):
+    """Exact law of MX.draw_token over both 32-bit words: the tile's interval probability
+    times the id's within the tile."""
+    off = (np.asarray(lmass_row, np.float32) - np.float32(lse)).astype(np.float32)
+    pt = _r_interval_probs(C.quant40(C.detexp32(off)))
+    law = np.zeros(len(tls_row))
+    for t, ptt in enumerate(pt):
+        ids = np.asarray(tls_row[t * MX.TILE:(t + 1) * MX.TILE], np.float32)
+        law[t * MX.TILE:t * MX.TILE + len(ids)] = ptt * _r_interval_probs(
+            C.quant40(C.detexp32(ids)))
+    return law
+
+
+@pytest.mark.parametrize("V", [128, 300, 1000])
+def test_two_stage_token_law_is_the_softmax(V):
+    """Drawing the tile from its mass, then the id within it, has the law softmax(logits) of
+    the whole row: within the binary32 rounding of the two-level form (relative), and within
+    the 2^-32 resolution of an inverse CDF driven by one 32-bit word, per stage (absolute)."""
+    rng = np.random.default_rng(V)
+    logits = rng.normal(size=V) * 3.0
+    logits[rng.integers(0, V, 5)] += 6.0   # a few dominant ids, in different tiles
+    q = np.exp(logits - logits.max())
+    q /= q.sum()
+    law = _token_law(*_two_level(logits))
+    assert abs(law.sum() - 1.0) < 1e-12
+    np.testing.assert_allclose(law, q, rtol=2e-6, atol=2 * 2.0 ** -32)
+
+
+def test_two_stage_draw_uses_both_words_and_the_tile_offset():
+    """Monte Carlo over many sequences: multi-tile rows give chi-square-consistent tokens, and
+    the ids drawn inside a tile follow its within-tile law (word 1 independent of word 0)."""
+    K, R, V, N = 1, 2, 300, 30000
+    rng = np.random.default_rng(7)
+    logits = rng.normal(size=(K, R, V)) * 1.5
+    tls, lmass, lse = _two_level(logits)
+    B = N
+    b3 = lambda a: np.broadcast_to(a, (B,) + a.shape)
+    ell = np.broadcast_to(np.array([0.3, -0.2], np.float32), (B, R))
+    z, x = MX.sample_blocks(b3(tls), b3(lmass), b3(lse), ell, 1.0, seed=19, step=5,
+                            seq=np.arange(N) + 7)
+    pi = MX.prior(ell[:1], 1.0)[0]
+    assert _chi2_pvalue(np.bincount(z, minlength=R), pi) > 1e-4
+    for zz in range(R):
+        sel = z == zz
+        q = np.exp(logits[0, zz] - logits[0, zz].max())
+        assert _chi2_pvalue(np.bincount(x[sel, 0], minlength=V), q / q.sum()) > 1e-4
+
+
+def test_two_stage_draw_single_tile_is_the_flat_inverse_cdf():
+    """A row of one tile: the tile stage is certain, so the token is the flat inverse CDF of
+    its quantised masses with word 1."""
+    rng = np.random.default_rng(3)
+    lq = _logsoftmax(rng.normal(size=100)).astype(np.float32)
+    for s in range(50):
+        r1 = C.draw_u32_word1(4, C.PURPOSE_TOKEN, 0, s, 2)
+        got = MX.draw_token(lq, np.zeros(1, np.float32), np.float32(0), C.draw_u32(
+            4, C.PURPOSE_TOKEN, 0, s, 2), r1)
+        assert got == C.icdf(C.quant40(C.detexp32(lq)), r1)
 
 
 # ---------------------------------------------------------------------------------------
@@ -191,7 +271,7 @@ def test_emitted_tokens_follow_the_target_monte_carlo():
     K, R, V, N = 2, 3, 5, 12000
     lq, ell, logp = tiny_case(53, N, K, R, V, q_scale=1.0, p_scale=1.0)
     seq = np.arange(N)
-    _, x = MX.sample_blocks(lq, ell, 1.0, seed=3, step=1, seq=seq)
+    _, x = MX.sample_blocks(*_one_tile(lq), ell, 1.0, seed=3, step=1, seq=seq)
     out = MX.verify_blocks(lq, ell, 1.0, x, logp, seed=3, step=1, seq=seq, with_beta=False)
     na, nt = out["n_accept"], out["next_token"]
     first = np.where(na >= 1, x[:, 0], nt)
@@ -231,7 +311,7 @@ def test_single_category_verify_is_textbook_speculative_sampling():
     logp = _logsoftmax(rng.normal(size=(N, K + 1, V)) * 0.7).astype(np.float32)
     ell = rng.normal(size=(N, 1)).astype(np.float32)
     seq = np.arange(N) + 1000
-    _, x = MX.sample_blocks(lq, ell, 1.0, seed=77, step=4, seq=seq)
+    _, x = MX.sample_blocks(*_one_tile(lq), ell, 1.0, seed=77, step=4, seq=seq)
     out = MX.verify_blocks(lq, ell, 1.0, x, logp, seed=77, step=4, seq=seq, with_beta=False)
     for b in range(N):
         n, t = _textbook_speculative_sampling(lq[b, :, 0], logp[b], x[b], 77, 4, int(seq[b]))
@@ -260,7 +340,7 @@ def test_full_acceptance_draws_the_bonus_token():
     logp = np.concatenate([lq[:, :, 0], _logsoftmax(rng.normal(size=(B, 1, V))).astype(np.float32)], 1)
     ell = np.zeros((B, 1), np.float32)
     seq = np.arange(B)
-    _, x = MX.sample_blocks(lq, ell, 1.0, seed=2, step=0, seq=seq)
+    _, x = MX.sample_blocks(*_one_tile(lq), ell, 1.0, seed=2, step=0, seq=seq)
     out = MX.verify_blocks(lq, ell, 1.0, x, logp, seed=2, step=0, seq=seq)
     assert np.all(out["n_accept"] == K)
     np.testing.assert_allclose(out["al"], K)
@@ -275,7 +355,7 @@ def test_zero_category_temperature_keeps_one_branch():
     B, K, R, V = 3, 4, 5, 12
     lq, ell, logp = tiny_case(91, B, K, R, V)
     top = int(np.argmax(ell[0]))
-    z, x = MX.sample_blocks(lq, ell, 0.0, seed=4, step=0, seq=np.arange(B))
+    z, x = MX.sample_blocks(*_one_tile(lq), ell, 0.0, seed=4, step=0, seq=np.arange(B))
     assert np.all(z == top)
     out = MX.verify_blocks(lq, ell, 0.0, x, logp, seed=4, step=0, seq=np.arange(B))
     want = np.zeros(R)
@@ -333,7 +413,7 @@ def test_monte_carlo_accepted_length_matches_enumeration():
     pi = MX.prior(ell[:1], 1.0)[0]
     exact = EN.exact_expected_al(_probs(lq[0]), pi, _probs(logp[0]))
     seq = np.arange(N)
-    _, x = MX.sample_blocks(lq, ell, 1.0, seed=11, step=3, seq=seq)
+    _, x = MX.sample_blocks(*_one_tile(lq), ell, 1.0, seed=11, step=3, seq=seq)
     out = MX.verify_blocks(lq, ell, 1.0, x, logp, seed=11, step=3, seq=seq, with_beta=False)
     for sample in (out["n_accept"].astype(np.float64), out["al"]):
         se = sample.std(ddof=1) / math.sqrt(N)
