@@ -755,10 +755,11 @@ def _step_run(wl, dev, mode, steps, warmup, with_inputs=False, settle_ms=0.0):
     per_step = sorted(e[0].elapsed_time(e[3]) for e in events)
     pct = {q: per_step[min(len(per_step) - 1, int(q / 100 * len(per_step)))] for q in (10, 50, 90)}
     # Algorithmic bytes: soft verify streams R branch rows + the target row per position; the
-    # soft draw one branch row per position. Greedy verify streams one target row per block
-    # (the first rejected position or the bonus row); the greedy draw reads no vocabulary row.
+    # soft draw reads, per position, the drawn branch row's tile masses and one 128-id tile
+    # (latency-bound). Greedy verify streams one target row per block (the first rejected
+    # position or the bonus row); the greedy draw reads no vocabulary row.
     verify_bytes = B * V * 4.0 if greedy else B * K * (R + 1) * V * 4.0
-    sample_bytes = 0.0 if greedy else B * K * V * 4.0
+    sample_bytes = 0.0 if greedy else B * K * (D.ntiles(V) + 128) * 4.0
     return {
         "value": B * K / (step_ms * 1e-3),
         "ms_per_step": step_ms,
@@ -767,8 +768,8 @@ def _step_run(wl, dev, mode, steps, warmup, with_inputs=False, settle_ms=0.0):
         "hbm": {"verify_GBps": verify_bytes / (verify_ms * 1e-3) / 1e9,
                 "verify_frac": verify_bytes / (verify_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
                 "verify_bytes": verify_bytes,
-                "sample_GBps": sample_bytes / (sample_ms * 1e-3) / 1e9,
-                "sample_frac": sample_bytes / (sample_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
+                "sample_bytes": sample_bytes,
+                "sample_bound": "latency"},
         "quality": {"mean_n_accept": float(vout["n_accept"].float().mean().item()),
                     "mean_exp_len": float(vout["exp_len"].float().mean().item()),
                     "mean_al_expected": float(vout["al_expected"].float().mean().item())},

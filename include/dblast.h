@@ -156,14 +156,18 @@ dbl_status dbl_head_logprobs(dbl_shape shape, int dt, const void* h, const void*
  * Block Drafting and Verification": first a category from the prior, then every position in
  * parallel from that branch). The prior is q_{Z_T}(z) = softmax(prior_logits[b, :] / z_temp)
  * (Sec. "Drafter sampling during inference"); z_temp = 0 selects the highest-prior category
- * (lowest index on ties).
+ * (lowest index on ties). Each token x_k ~ q_k(. | z) is drawn in two stages on the head's
+ * two-level form: its 128-id tile with probability exp(lmass_t - lse), then the id within the
+ * tile with probability exp(tls_v) (their product is q_k(v | z)); each stage is an exact
+ * inverse CDF on probabilities quantised to 2^-40, driven by Philox words 0 and 1.
  *   tls, lmass, lse   the head output for this batch (shape.d is unused)
  *   prior_logits      [B, R] fp32 category logits l_z(y)
  *   z_temp            category temperature Z_T >= 0
  *   seed, step        Philox key and step counter; seq_offset + b is block b's sequence index
  *   z_out  out [B] int32 drawn category;  x_out  out [B, K] int32 drafted tokens
  * A row whose quantised probabilities are all zero yields token -1.
- * Errors: DBL_EINVAL for null pointers or z_temp < 0 or NaN; DBL_EWORKSPACE; DBL_ESHAPE.
+ * No workspace (dbl_workspace_bytes(DBL_OP_SAMPLE, .) = 0): ws may be NULL with ws_bytes 0.
+ * Errors: DBL_EINVAL for null pointers or z_temp < 0 or NaN; DBL_ESHAPE.
  */
 dbl_status dbl_sample_block(dbl_shape shape, const float* tls, const float* lmass,
                             const float* lse, const float* prior_logits, float z_temp,

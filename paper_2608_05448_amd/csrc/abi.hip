@@ -84,8 +84,7 @@ WsLayout layout(int op, const dbl_shape& s) {
       n = 1;
       break;
     case DBL_OP_SAMPLE:
-      sizes[0] = B * K * nT * sizeof(uint64_t);
-      n = 1;
+      n = 0;
       break;
     case DBL_OP_VERIFY:
       sizes[0] = B * K * R * sizeof(double);
@@ -331,7 +330,6 @@ dbl_status dbl_sample_block(dbl_shape s, const float* tls, const float* lmass,
   a.blk = block_args(s, tls, lmass, lse, prior_logits, z_temp, seed, step, seq_offset);
   a.z_out = z_out;
   a.x_out = x_out;
-  a.tilesum = reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + L.off[0]);
   return hip_status(dbl::launch_sample(a, static_cast<hipStream_t>(stream)), "sample launch");
 }
 

@@ -19,8 +19,12 @@ namespace dbl {
 // ---------------------------------------------------------------------------------------
 enum Purpose : uint32_t { kCategory = 0, kToken = 1, kAccept = 2, kResidual = 3 };
 
-__device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint32_t c2,
-                                                 uint32_t c3, uint32_t k0, uint32_t k1) {
+struct PhiloxPair {
+  uint32_t w0, w1;  // output words 0 and 1 of one Philox4x32-10 block
+};
+
+__device__ __forceinline__ PhiloxPair philox_words01(uint32_t c0, uint32_t c1, uint32_t c2,
+                                                     uint32_t c3, uint32_t k0, uint32_t k1) {
   constexpr uint32_t kM0 = 0xD2511F53u, kM1 = 0xCD9E8D57u;
   constexpr uint32_t kW0 = 0x9E3779B9u, kW1 = 0xBB67AE85u;
 #pragma unroll
@@ -36,7 +40,12 @@ __device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint3
     k0 += kW0;
     k1 += kW1;
   }
-  return c0;
+  return {c0, c1};
+}
+
+__device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint32_t c2,
+                                                 uint32_t c3, uint32_t k0, uint32_t k1) {
+  return philox_words01(c0, c1, c2, c3, k0, k1).w0;
 }
 
 // The uniform word for (purpose, position k) of sequence `seq` at `step` under `seed`.
@@ -44,6 +53,14 @@ __device__ __forceinline__ uint32_t draw(uint64_t seed, uint32_t purpose, uint32
                                          uint64_t seq, uint64_t step) {
   return philox_word0(k, purpose, static_cast<uint32_t>(seq), static_cast<uint32_t>(step),
                       static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32));
+}
+
+// Words 0 and 1 of the same block: the drafted token's tile (word 0) and its id within the
+// tile (word 1).
+__device__ __forceinline__ PhiloxPair draw2(uint64_t seed, uint32_t purpose, uint32_t k,
+                                            uint64_t seq, uint64_t step) {
+  return philox_words01(k, purpose, static_cast<uint32_t>(seq), static_cast<uint32_t>(step),
+                        static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32));
 }
 
 // ---------------------------------------------------------------------------------------

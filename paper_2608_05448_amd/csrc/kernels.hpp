@@ -40,7 +40,6 @@ struct SampleArgs {
   BlockArgs blk;
   int32_t* z_out;
   int32_t* x_out;
-  uint64_t* tilesum;  // workspace [B*K, nT]
 };
 
 struct VerifyArgs {

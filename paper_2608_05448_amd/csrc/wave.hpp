@@ -246,4 +246,49 @@ __device__ int select_by_tiles_block(const uint64_t* tiles, int nT, int64_t V, u
   return res == ~0ull ? -1 : static_cast<int>(res);
 }
 
+// Inverse CDF over n integer weights weight(0..n-1) by a 256-thread workgroup (every thread
+// calls it, with the same n and r): each thread sums a contiguous run, a workgroup scan gives
+// the total Z and the run holding the threshold T = floor(r Z / 2^32), and that run's thread
+// finds the smallest index whose inclusive cumulative weight exceeds T. Returns -1 when Z = 0.
+// `lds` must hold 8 uint64; weight(i) is called twice for the indices of the selected run.
+template <class WeightFn>
+__device__ int select_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid >> 6;
+  const int per = (n + 255) / 256;
+  const int i0 = min(n, tid * per), i1 = min(n, i0 + per);
+  uint64_t part = 0;
+  for (int i = i0; i < i1; ++i) part += weight(i);
+  uint64_t incl = wave_incl_scan_u64(part);
+  if (lane == 63) lds[wave] = incl;
+  __syncthreads();
+  uint64_t base = 0, Z = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (w < wave) base += lds[w];
+    Z += lds[w];
+  }
+  __syncthreads();
+  if (Z == 0) return -1;
+  const uint64_t T = icdf_threshold(r, Z);
+  incl += base;
+  const uint64_t excl = incl - part;
+  if (excl <= T && T < incl) {  // exactly one thread's run holds the threshold
+    uint64_t c = excl;
+    for (int i = i0; i < i1; ++i) {
+      const uint64_t wi = weight(i);
+      if (c + wi > T) {
+        lds[4] = static_cast<uint64_t>(i);
+        break;
+      }
+      c += wi;
+    }
+  }
+  __syncthreads();
+  const int res = static_cast<int>(lds[4]);
+  __syncthreads();
+  return res;
+}
+
 }  // namespace dbl

@@ -64,14 +64,22 @@ class BlockCase:
 _ORACLE_FULL: dict = {}
 
 
-def oracle_full_head(name: str, h: torch.Tensor, w: torch.Tensor) -> np.ndarray:
-    """The oracle's branch log-probs [M, V] (binary32 flat form) for a whole workload's head,
-    from the exact inputs h [B, K, R, d] and w [V, d] the GPU consumed (binary64 GEMM and
-    log-softmax). Computed once per process for the most recent workload name."""
+def _oracle_full(name: str, h: torch.Tensor, w: torch.Tensor):
     if name not in _ORACLE_FULL:
         _ORACLE_FULL.clear()
         d = h.shape[-1]
         tls, lmass, lse = OH.head_factored(np32(h).reshape(-1, d), np32(w), v_chunk=8192)
-        _ORACLE_FULL[name] = OH.flat_logq(tls, lmass, lse)
-        del tls, lmass, lse
+        _ORACLE_FULL[name] = (tls, lmass, lse, OH.flat_logq(tls, lmass, lse))
     return _ORACLE_FULL[name]
+
+
+def oracle_full_head(name: str, h: torch.Tensor, w: torch.Tensor) -> np.ndarray:
+    """The oracle's branch log-probs [M, V] (binary32 flat form) for a whole workload's head,
+    from the exact inputs h [B, K, R, d] and w [V, d] the GPU consumed (binary64 GEMM and
+    log-softmax). Computed once per process for the most recent workload name."""
+    return _oracle_full(name, h, w)[3]
+
+
+def oracle_full_factored(name: str, h: torch.Tensor, w: torch.Tensor):
+    """The same head in its binary32 two-level form (tls [M, V], lmass [M, nT], lse [M])."""
+    return _oracle_full(name, h, w)[:3]

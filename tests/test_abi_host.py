@@ -52,9 +52,8 @@ def test_workspace_sizes(lib):
     g = lib.dbl_workspace_bytes(D.DBL_OP_VERIFY_GREEDY, S(16, 16, 8, 0, 151936))
     assert g == 2048 * 8 + 2 * -(-16 * 1187 * 8 // 256) * 256
     assert lib.dbl_workspace_bytes(D.DBL_OP_EXPECTED_LEN_GREEDY, S(16, 16, 8, 0, 151936)) == 2048 * 8
-    # Sample: one uint64 per (position, tile).
-    assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, S(16, 16, 8, 0, 151936)) == \
-        -(-16 * 16 * 1187 * 8 // 256) * 256
+    # Sample: no workspace (the two-stage draw reads the tile masses directly).
+    assert lib.dbl_workspace_bytes(D.DBL_OP_SAMPLE, S(16, 16, 8, 0, 151936)) == 0
     v = lib.dbl_workspace_bytes(D.DBL_OP_VERIFY, S(16, 16, 8, 0, 151936))
     e = lib.dbl_workspace_bytes(D.DBL_OP_EXPECTED_LEN, S(16, 16, 8, 0, 151936))
     assert v > e > 0 and v % 256 == 0 and e % 256 == 0
@@ -147,14 +146,6 @@ def test_sample_and_verify_validation(lib):
     for zt in (-0.5, float("nan"), float("inf")):
         assert lib.dbl_sample_block(shape, p[0], p[1], p[2], p[3], zt, 0, 0, 0, p[4], p[5],
                                     aligned, ws_need, null) == D.DBL_EINVAL
-    # Workspace: missing, too small, misaligned.
-    assert lib.dbl_sample_block(shape, p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4], p[5],
-                                null, ws_need, null) == D.DBL_EWORKSPACE
-    assert lib.dbl_sample_block(shape, p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4], p[5],
-                                aligned, ws_need - 1, null) == D.DBL_EWORKSPACE
-    assert lib.dbl_sample_block(shape, p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4], p[5],
-                                ctypes.c_void_p(0x100010), ws_need, null) == D.DBL_EWORKSPACE
-    assert "256-byte" in _err(lib)
     # Too many categories.
     assert lib.dbl_sample_block(S(2, 4, 65, 0, 300), p[0], p[1], p[2], p[3], 1.0, 0, 0, 0, p[4],
                                 p[5], aligned, 1 << 30, null) == D.DBL_ESHAPE

@@ -22,11 +22,18 @@ from oracle import mixture as MX
 pytestmark = pytest.mark.gpu
 
 
-def _oracle_lq(h_block, w_np):
-    """Oracle branch log-probs [K, R, V] (binary32 flat form) for one block's hidden states."""
+def _oracle_factored(h_block, w_np):
+    """Oracle branch log-probs of one block's hidden states, in the two-level form
+    (tls [K, R, V], lmass [K, R, nT], lse [K, R]) and flat (lq [K, R, V]), binary32."""
     K, R, d = h_block.shape
     tls, lm, ls = OH.head_factored(np32(h_block).reshape(K * R, d), w_np, v_chunk=8192)
-    return OH.flat_logq(tls, lm, ls).reshape(K, R, -1)
+    lq = OH.flat_logq(tls, lm, ls).reshape(K, R, -1)
+    return tls.reshape(K, R, -1), lm.reshape(K, R, -1), ls.reshape(K, R), lq
+
+
+def _oracle_lq(h_block, w_np):
+    """Oracle branch log-probs [K, R, V] (binary32 flat form) for one block's hidden states."""
+    return _oracle_factored(h_block, w_np)[3]
 
 
 def _rel(a, b):
@@ -35,11 +42,11 @@ def _rel(a, b):
     return float(np.max(np.abs(a[m] - b[m]) / np.abs(b[m]))) if m.any() else 0.0
 
 
-def _near_tie_token(lq_row, r, got, want):
-    """True if the GPU token `got` differs from the oracle's `want` only because the threshold
-    sits within a relative 1e-5 of the cumulative boundary between them."""
-    q = C.quant40(C.detexp32(lq_row))
-    cum = np.cumsum(q.astype(np.float64))
+def _near_tie(weights, r, got, want):
+    """True if an inverse CDF on integer `weights` with word r picks `got` instead of `want`
+    only because its threshold sits within a relative 1e-5 of the cumulative boundary between
+    them."""
+    cum = np.cumsum(np.asarray(weights).astype(np.float64))
     Z = cum[-1]
     T = (int(r) * int(Z)) >> 32
     lo, hi = min(got, want), max(got, want)
@@ -47,10 +54,21 @@ def _near_tie_token(lq_row, r, got, want):
     return gap <= 1e-5 * Z
 
 
+def _near_tie_token(tls_row, lm_row, ls, r_tile, r_id, got, want):
+    """The two-stage draw of a token: a near-tie in the tile stage when the tiles differ, else
+    in the id stage within their common tile."""
+    tg, tw = got // MX.TILE, want // MX.TILE
+    if tg != tw:
+        off = (np.asarray(lm_row, np.float32) - np.float32(ls)).astype(np.float32)
+        return _near_tie(C.quant40(C.detexp32(off)), r_tile, tg, tw)
+    ids = np.asarray(tls_row[tw * MX.TILE:(tw + 1) * MX.TILE], np.float32)
+    return _near_tie(C.quant40(C.detexp32(ids)), r_id, got % MX.TILE, want % MX.TILE)
+
+
 def test_e2e_qwen3_8b_all_blocks_all_temperatures():
     """The benchmark's step at the Qwen3-8B shape, every block: the oracle's binary64 head on the
     same bf16 inputs, then its own draw and verification, at every target temperature."""
-    from cases import oracle_full_head
+    from cases import oracle_full_factored, oracle_full_head
     from paper_2608_05448_amd import dblast as D
     wl = synth.WORKLOADS["qwen3_8b"]
     print(f"[fullsize] qwen3_8b e2e B={wl.B} K={wl.K} R={wl.R} d={wl.d} V={wl.V}", flush=True)
@@ -63,16 +81,22 @@ def test_e2e_qwen3_8b_all_blocks_all_temperatures():
     B, K, R, V = wl.B, wl.K, wl.R, wl.V
     print(f"[fullsize] qwen3_8b: oracle head on all {wl.M} rows", flush=True)
     lq_all = oracle_full_head("qwen3_8b", h, w).reshape(B, K, R, V)
+    o_tls, o_lm, o_ls = oracle_full_factored("qwen3_8b", h, w)
+    o_tls, o_lm, o_ls = o_tls.reshape(B, K, R, V), o_lm.reshape(B, K, R, -1), o_ls.reshape(B, K, R)
     z_g, x_g = z.cpu().numpy(), x.cpu().numpy()
     ell_np = ell.cpu().numpy()
-    z_o, x_o = MX.sample_blocks(lq_all, ell_np, wl.z_temp, wl.philox_seed, 0, np.arange(B))
+    z_o, x_o = MX.sample_blocks(o_tls, o_lm, o_ls, ell_np, wl.z_temp, wl.philox_seed, 0,
+                                np.arange(B))
     np.testing.assert_array_equal(z_g, z_o)
     mismatches = 0
     for b in range(B):
         for k in range(K):
             if x_g[b, k] != x_o[b, k]:
-                r = C.draw_u32(wl.philox_seed, C.PURPOSE_TOKEN, k, b, 0)
-                assert _near_tie_token(lq_all[b, k, z_o[b]], r, x_g[b, k], x_o[b, k])
+                r0 = C.draw_u32(wl.philox_seed, C.PURPOSE_TOKEN, k, b, 0)
+                r1 = C.draw_u32_word1(wl.philox_seed, C.PURPOSE_TOKEN, k, b, 0)
+                zb = z_o[b]
+                assert _near_tie_token(o_tls[b, k, zb], o_lm[b, k, zb], o_ls[b, k, zb], r0, r1,
+                                       x_g[b, k], x_o[b, k])
                 mismatches += 1
     print(f"[fullsize] qwen3_8b draw: certified near-ties {mismatches}", flush=True)
     # Verification is compared where both sides drafted the same block (all of them unless a
@@ -195,10 +219,10 @@ def test_stress_workload_1000_step_loop():
     ell_np = ell.cpu().numpy()
     lp = logp.cpu().numpy()
     for b in probe_blocks:
-        lq = _oracle_lq(h[b], w_np)
+        o_tls, o_lm, o_ls, lq = _oracle_factored(h[b], w_np)
         for t in probe_steps:
-            zo, xo = MX.sample_blocks(lq[None], ell_np[b:b + 1], wl.z_temp, wl.philox_seed, t,
-                                      np.array([b]))
+            zo, xo = MX.sample_blocks(o_tls[None], o_lm[None], o_ls[None], ell_np[b:b + 1],
+                                      wl.z_temp, wl.philox_seed, t, np.array([b]))
             zg, xg, nag, ntg = (a[b] for a in rec[t])
             assert zg == zo[0]
             assert np.array_equal(xg, xo[0]), (b, t)

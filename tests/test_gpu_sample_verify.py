@@ -67,7 +67,7 @@ def test_sample_verify_parity(case):
     z_g, x_g = D.dbl_sample_block(tls, lmass, lse, ell, z_temp=zt, seed=seed, step=step,
                                   seq_offset=so)
     torch.cuda.synchronize()
-    z_o, x_o = MX.sample_blocks(c.lq, c.ell, zt, seed, step, seq)
+    z_o, x_o = MX.sample_blocks(c.tls, c.lmass, c.lse, c.ell, zt, seed, step, seq)
     np.testing.assert_array_equal(z_g.cpu().numpy(), z_o)
     np.testing.assert_array_equal(x_g.cpu().numpy(), x_o)
 
@@ -123,7 +123,7 @@ def test_accept_paths_at_the_benchmark_variants(R, K):
     z, x = D.dbl_sample_block(tls, lmass, lse, ell, seed=3, step=1)
     out = D.dbl_verify_block(tls, lmass, lse, ell, x, logp, seed=3, step=1)
     torch.cuda.synchronize()
-    z_o, x_o = MX.sample_blocks(c.lq, c.ell, 1.0, 3, 1, seq)
+    z_o, x_o = MX.sample_blocks(c.tls, c.lmass, c.lse, c.ell, 1.0, 3, 1, seq)
     np.testing.assert_array_equal(z.cpu().numpy(), z_o)
     np.testing.assert_array_equal(x.cpu().numpy(), x_o)
     ref = MX.verify_blocks(c.lq, c.ell, 1.0, x_o, c.logp, 3, 1, seq)
