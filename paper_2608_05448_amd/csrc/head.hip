@@ -1300,6 +1300,8 @@ __global__ __launch_bounds__(256) void zero_u64_kernel(uint64_t* __restrict__ p,
   if (i < n) p[i] = 0;
 }
 
+constexpr int kLseRegs = 32;
+
 // lse[m] = log sum_t exp(lmass[m, t]); one wave per row. With argmax requested, also decodes
 // the row's winning key into the vocabulary id.
 __global__ __launch_bounds__(256) void lse_finalize_kernel(const float* __restrict__ lmass,
@@ -1311,20 +1313,40 @@ __global__ __launch_bounds__(256) void lse_finalize_kernel(const float* __restri
   const int lane = threadIdx.x & 63;
   if (m >= M) return;
   const float* row = lmass + m * nT;
-  // Two passes over the row (the second from cache): the maximum, then the sum of exponentials
-  // relative to it; the loads of a pass are independent, so they overlap.
-  float mx = -INFINITY;
-#pragma unroll 4
-  for (int t = lane; t < nT; t += 64) mx = fmaxf(mx, row[t]);
-  const float gmx = wave_max(mx);
-  float s = 0.0f;
-  if (gmx > -INFINITY) {
-#pragma unroll 4
-    for (int t = lane; t < nT; t += 64) {
-      const float x = row[t];
-      s += x > -INFINITY ? __expf(x - gmx) : 0.0f;
+  // The maximum, then the sum of exponentials relative to it, each lane over ids lane, lane +
+  // 64, ... in that order. Rows of up to 64 kLseRegs tiles (V <= 262,144) are loaded once, all
+  // loads issued together, and kept in registers for both passes; longer rows are read twice.
+  float mx = -INFINITY, s = 0.0f;
+  if (nT <= 64 * kLseRegs) {
+    float x[kLseRegs];
+#pragma unroll
+    for (int i = 0; i < kLseRegs; ++i) {
+      const int t = lane + 64 * i;
+      x[i] = t < nT ? row[t] : -INFINITY;
     }
+#pragma unroll
+    for (int i = 0; i < kLseRegs; ++i) mx = fmaxf(mx, x[i]);
+    const float gmx = wave_max(mx);
+    if (gmx > -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < kLseRegs; ++i)
+        if (lane + 64 * i < nT) s += x[i] > -INFINITY ? __expf(x[i] - gmx) : 0.0f;
+    }
+    mx = gmx;
+  } else {
+#pragma unroll 4
+    for (int t = lane; t < nT; t += 64) mx = fmaxf(mx, row[t]);
+    const float gmx = wave_max(mx);
+    if (gmx > -INFINITY) {
+#pragma unroll 4
+      for (int t = lane; t < nT; t += 64) {
+        const float x = row[t];
+        s += x > -INFINITY ? __expf(x - gmx) : 0.0f;
+      }
+    }
+    mx = gmx;
   }
+  const float gmx = mx;
   s = wave_sum(s);
   if (lane == 0) {
     lse[m] = gmx + __logf(s);

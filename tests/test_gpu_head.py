@@ -68,6 +68,7 @@ def test_head_fp32_ragged(B, K, R, d, V):
     (1, 16, 8, 192, 4100),   # three 64-deep stages (odd count) in the register-staged kernel
     (9, 16, 8, 128, 3000),   # five branch-row tiles: more than one group of the tile order
     (9, 16, 8, 96, 3000),    # the same with the direct-to-LDS kernel
+    (1, 1, 3, 64, 270000),   # more than 2048 tiles per row: the LSE pass reads the row twice
 ])
 def test_head_bf16_ragged(B, K, R, d, V):
     h = synth.make_uniform_logits((B, K, R, d), 21).to(torch.bfloat16)
