@@ -159,27 +159,6 @@ __device__ __forceinline__ uint64_t quant_detexp32(float x) {
   const int amt = min(127 - static_cast<int>(u >> 23) - static_cast<int>(n), 63);
   return t >> amt;
 }
-// The same integer as quant_detexp32(x), as a binary64 value (exact: it is below 2^41), for
-// exact sums in binary64 of up to 2^12 of them: floor(p 2^(n + 40)) with the scaling by 2^(n + 40)
-// exact while the product is normal (a subnormal one is below 1 and floors to 0).
-__device__ __forceinline__ double quant_detexp32_d(float x) {
-#pragma clang fp contract(off)
-  x = fminf(fmaxf(x, -100.0f), 0.0f);
-  constexpr float kLog2e = 0x1.715476p+0f;
-  constexpr float kLn2Hi = 0x1.62e4p-1f;
-  constexpr float kLn2Lo = 0x1.7f7d1cp-20f;
-  const float n = rintf(__fmul_rn(x, kLog2e));
-  const float r = __fsub_rn(__fsub_rn(x, __fmul_rn(n, kLn2Hi)), __fmul_rn(n, kLn2Lo));
-  float p = static_cast<float>(1.0 / 5040.0);
-  p = __fadd_rn(__fmul_rn(p, r), static_cast<float>(1.0 / 720.0));
-  p = __fadd_rn(__fmul_rn(p, r), static_cast<float>(1.0 / 120.0));
-  p = __fadd_rn(__fmul_rn(p, r), static_cast<float>(1.0 / 24.0));
-  p = __fadd_rn(__fmul_rn(p, r), static_cast<float>(1.0 / 6.0));
-  p = __fadd_rn(__fmul_rn(p, r), 0.5f);
-  p = __fadd_rn(__fmul_rn(p, r), 1.0f);
-  p = __fadd_rn(__fmul_rn(p, r), 1.0f);
-  return static_cast<double>(floorf(ldexpf(p, static_cast<int>(n) + 40)));
-}
 __device__ __forceinline__ uint64_t quant40d(double y) {
   return static_cast<uint64_t>(y * 0x1p40);
 }
