@@ -1,6 +1,7 @@
 // Test helper (not part of the library): checks on the GPU, for every one of the 2^32 binary32
 // bit patterns, that the branch-free quantised exponential the sampler and verifier use equals the
-// determinism contract's definition quant40(detexp32(x)) = floor(detexp32(x) 2^40).
+// determinism contract's definition quant40(detexp32(x)) = floor(detexp32(x) 2^40); and evaluates
+// the kernels' Philox4x32-10 (output words 0 and 1) on given counters and keys.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -30,7 +31,24 @@ __global__ __launch_bounds__(256) void quant_all_kernel(unsigned long long* bad,
   }
 }
 
+__global__ __launch_bounds__(64) void philox01_kernel(const uint32_t* in, uint32_t* out, int n) {
+  const int i = blockIdx.x * 64 + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t* w = in + 6 * i;
+  const dbl::PhiloxPair r = dbl::philox_words01(w[0], w[1], w[2], w[3], w[4], w[5]);
+  out[2 * i] = r.w0;
+  out[2 * i + 1] = r.w1;
+}
+
 }  // namespace
+
+// in: device [n, 6] u32 (counter words 0..3, key words 0..1); out: device [n, 2] u32.
+extern "C" int dbl_test_philox01(const uint32_t* in, uint32_t* out, int n, void* stream) {
+  if (n <= 0) return 0;
+  hipLaunchKernelGGL(philox01_kernel, dim3((n + 63) / 64), dim3(64), 0,
+                     static_cast<hipStream_t>(stream), in, out, n);
+  return static_cast<int>(hipGetLastError());
+}
 
 // bad: device u64, zeroed by the caller; first: device u32, set to 0xffffffff by the caller.
 extern "C" int dbl_test_quant_exhaustive(unsigned long long* bad, unsigned* first, void* stream) {
