@@ -326,27 +326,30 @@ __device__ __forceinline__ int xcd_remap(int id, int n) {
 }
 
 // Logical tile id -> (vocabulary tile, branch-row tile). Branch-row tiles are taken in groups
-// of up to kGroupM; a group sweeps every vocabulary tile before the next group starts, and
-// within a vocabulary tile the group's branch-row tiles are consecutive. With groups of 4, the
-// ~32 workgroups resident on one XCD cover about 8 vocabulary x 4 branch-row tiles: each slab of
-// w is read by up to 4 of them and each slab of h by about 8, from that XCD's L2 (measured ~1%
-// faster than groups of 8 at the Qwen3-8B shape, 3% faster than no grouping).
-#ifndef DBL_HEAD_GROUPM
-#define DBL_HEAD_GROUPM 4
-#endif
-constexpr int kGroupM = DBL_HEAD_GROUPM;
+// of up to g; a group sweeps every vocabulary tile before the next group starts, and within a
+// vocabulary tile the group's branch-row tiles are consecutive. With groups of 4, the ~32
+// workgroups resident on one XCD cover about 8 vocabulary x 4 branch-row tiles: each slab of w
+// is read by up to 4 of them and each slab of h by about 8, from that XCD's L2. Measured: groups
+// of 4 are 1% faster than 8 at 8 branch-row tiles (the Qwen3-8B head) and 1.7% at 32 (B = 256,
+// K = 8, R = 4), 3% faster than no grouping; with 128 branch-row tiles (a 128-block chunk at
+// K = R = 16, where each group re-streams all of w from HBM) groups of 8 are 1.7% faster than 4
+// and groups of 16 or 32 slower.
+constexpr int kGroupM = 4;
+constexpr int kGroupMLarge = 8;      // from kGroupLargeFrom branch-row tiles up
+constexpr int kGroupLargeFrom = 64;
 __device__ __forceinline__ void tile_of(int L, int n_vtiles, int n_mtiles, int* vt, int* mt) {
-  const int n_groups = (n_mtiles + kGroupM - 1) / kGroupM;
-  const int per_full = n_vtiles * kGroupM;
+  const int gm = n_mtiles >= kGroupLargeFrom ? kGroupMLarge : kGroupM;
+  const int n_groups = (n_mtiles + gm - 1) / gm;
+  const int per_full = n_vtiles * gm;
   if (L < (n_groups - 1) * per_full) {
     const int g = L / per_full, rem = L % per_full;
-    *vt = rem / kGroupM;
-    *mt = g * kGroupM + rem % kGroupM;
+    *vt = rem / gm;
+    *mt = g * gm + rem % gm;
   } else {
     const int rem = L - (n_groups - 1) * per_full;
-    const int gl = n_mtiles - (n_groups - 1) * kGroupM;
+    const int gl = n_mtiles - (n_groups - 1) * gm;
     *vt = rem / gl;
-    *mt = (n_groups - 1) * kGroupM + rem % gl;
+    *mt = (n_groups - 1) * gm + rem % gl;
   }
 }
 

@@ -69,6 +69,7 @@ def test_head_fp32_ragged(B, K, R, d, V):
     (9, 16, 8, 128, 3000),   # five branch-row tiles: more than one group of the tile order
     (9, 16, 8, 96, 3000),    # the same with the direct-to-LDS kernel
     (1, 1, 3, 64, 270000),   # more than 2048 tiles per row: the LSE pass reads the row twice
+    (65, 16, 16, 64, 600),   # 65 branch-row tiles: the tile order's groups of 8, a partial last group
 ])
 def test_head_bf16_ragged(B, K, R, d, V):
     h = synth.make_uniform_logits((B, K, R, d), 21).to(torch.bfloat16)
