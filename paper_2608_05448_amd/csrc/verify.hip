@@ -545,13 +545,24 @@ constexpr float kLog2eChunk = 1.4426950408889634f;
 template <int RT>
 constexpr int stream_waves() { return RT > 8 ? 6 : 8; }
 
+// Chunks per workgroup: a chunk streams (R + 1) x 16 KB per position row, so at R <= 4 several
+// chunks share a workgroup's start-up when the grid stays large (stress shape, R = 4: 1.157 ->
+// 1.088 ms with four, 1.009 with eight, 1.008 with sixteen, 1.230 with all 37 in one); at R = 8
+// a chunk loop measured 6% slower even at one chunk, so R > 4 keeps one chunk per workgroup
+// and no loop.
+constexpr int kStreamChunksSmallR = 8;
+constexpr int64_t kStreamMinGroups = 2048;  // one workgroup per slot at eight waves per SIMD
+__host__ __device__ constexpr bool stream_multi_chunk(int rt) { return rt > 0 && rt <= 4; }
+
 template <int RT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(stream_waves<RT>(), 8)))
-void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
+void verify_stream_kernel(VerifyArgs a, int nchunk, int rows, int cpw) {
+  const int CPW = stream_multi_chunk(RT) ? cpw : 1;
   const BlockArgs& k_ = a.blk;
   const int64_t B = k_.B;
-  const int c = static_cast<int>(blockIdx.x % static_cast<unsigned>(nchunk));
-  const int64_t pb = blockIdx.x / static_cast<unsigned>(nchunk);
+  const int ncw = (nchunk + CPW - 1) / CPW;
+  const int cw = static_cast<int>(blockIdx.x % static_cast<unsigned>(ncw));
+  const int64_t pb = blockIdx.x / static_cast<unsigned>(ncw);
   const int64_t k = pb / B, b = pb % B;
   const int R = RT > 0 ? RT : static_cast<int>(k_.R);
   const int64_t V = k_.V;
@@ -564,15 +575,20 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
   const int ks = a.trajectory ? -1 : a.n_accept[b];  // first rejected position, K if none
   const bool bonus = k == k_.K;
   const bool res = !a.trajectory && (bonus ? ks == k_.K : k == ks);
+  const int64_t m0 = (b * k_.K + k) * k_.R;  // first branch row of the position (k < K)
+#pragma unroll 1
+  for (int cc = 0; cc < CPW; ++cc) {
+  const int c = cw * CPW + cc;
+  if (c >= nchunk) break;       // workgroup-uniform
+  if (cc > 0) __syncthreads();  // the previous chunk's readers of s_offx and red are done
   const int t0 = c * kTilesPerChunk;
   const int nt = min(kTilesPerChunk, k_.nT - t0);
-  const int64_t m0 = (b * k_.K + k) * k_.R;  // first branch row of the position (k < K)
   if (!bonus) {
     for (int i = tid; i < R * kTilesPerChunk; i += blockDim.x) {
       const int z = i / kTilesPerChunk, tt = i % kTilesPerChunk;
       if (tt < nt) s_offx[z][tt] = k_.lmass[(m0 + z) * k_.nT + t0 + tt] - k_.lse[m0 + z];
     }
-    if (tid < R) {
+    if (cc == 0 && tid < R) {
       const double wv = a.wpost[m0 + tid];
       s_w[tid] = static_cast<float>(wv);
       s_wz[tid] = wv;
@@ -682,6 +698,7 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
                          (red[0] + red[1]) + (red[2] + red[3]), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
   }
+  }
   // Arrival. The partials above are device-coherent stores (written through the XCD's L2); each
   // wave waits until its own have completed before the count is taken, so a workgroup that
   // sees the final count sees every partial of the block once it has dropped its cached lines
@@ -690,7 +707,7 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows) {
   __syncthreads();
   if (tid == 0)
     s_last = __hip_atomic_fetch_add(a.arrive + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-             static_cast<uint32_t>(rows) * nchunk - 1u;
+             static_cast<uint32_t>(rows) * ncw - 1u;
   __syncthreads();
   if (!s_last) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -717,16 +734,21 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
     // mode keeps the two launches below: its stream kernel has no residual arithmetic to carry,
     // and at R = 16 it measured 3.48 ms against 3.78 ms fused per 128-block chunk.
     const int rows = static_cast<int>(a.blk.K) + (!a.trajectory && a.Kp == a.blk.K + 1 ? 1 : 0);
-    const int64_t nwg = static_cast<int64_t>(rows) * B * nchunk;
+    const int64_t R = a.blk.R;  // the template argument of the launch below: R, or 0
+    const int rt = R == 1 || R == 2 || R == 4 || R == 8 || R == 16 ? static_cast<int>(R) : 0;
+    const int64_t cw_many = (nchunk + kStreamChunksSmallR - 1) / kStreamChunksSmallR;
+    const int cpw = stream_multi_chunk(rt) && rows * B * cw_many >= kStreamMinGroups
+                        ? kStreamChunksSmallR : 1;
+    const int64_t nwg = static_cast<int64_t>(rows) * B * ((nchunk + cpw - 1) / cpw);
     if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nwg));
     switch (a.blk.R) {
-      case 1: hipLaunchKernelGGL(verify_stream_kernel<1>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
-      case 2: hipLaunchKernelGGL(verify_stream_kernel<2>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
-      case 4: hipLaunchKernelGGL(verify_stream_kernel<4>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
-      case 8: hipLaunchKernelGGL(verify_stream_kernel<8>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
-      case 16: hipLaunchKernelGGL(verify_stream_kernel<16>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
-      default: hipLaunchKernelGGL(verify_stream_kernel<0>, grid, dim3(256), 0, stream, a, nchunk, rows); break;
+      case 1: hipLaunchKernelGGL(verify_stream_kernel<1>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
+      case 2: hipLaunchKernelGGL(verify_stream_kernel<2>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
+      case 4: hipLaunchKernelGGL(verify_stream_kernel<4>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
+      case 8: hipLaunchKernelGGL(verify_stream_kernel<8>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
+      case 16: hipLaunchKernelGGL(verify_stream_kernel<16>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
+      default: hipLaunchKernelGGL(verify_stream_kernel<0>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
     }
     return hipGetLastError();
   }

@@ -109,6 +109,34 @@ def test_accept_paths_are_exercised():
     assert (na == 0).any() and ((na > 0) & (na < 4)).any() and (na == 4).any(), na
 
 
+def test_stream_several_chunks_per_workgroup():
+    """R = 4 with a grid large enough that each stream workgroup takes several 32-tile chunks
+    (256 blocks, 8 position rows, 5 chunks of which the last is partial, all in one workgroup):
+    every output against the oracle, with all accept paths."""
+    from paper_2608_05448_amd import dblast as D
+    B, K, R, V = 256, 7, 4, 20000
+    print(f"[sample/verify] several chunks per workgroup R={R} K={K} B={B} V={V}", flush=True)
+    c = BlockCase(B, K, R, V, d=16, seed=77, target="aligned-block", kp_extra=1, noise=0.1)
+    tls, lmass, lse, ell, logp = c.device()
+    seq = np.arange(B)
+    z, x = D.dbl_sample_block(tls, lmass, lse, ell, seed=5, step=2)
+    out = D.dbl_verify_block(tls, lmass, lse, ell, x, logp, seed=5, step=2)
+    torch.cuda.synchronize()
+    z_o, x_o = MX.sample_blocks(c.tls, c.lmass, c.lse, c.ell, 1.0, 5, 2, seq)
+    np.testing.assert_array_equal(z.cpu().numpy(), z_o)
+    np.testing.assert_array_equal(x.cpu().numpy(), x_o)
+    ref = MX.verify_blocks(c.lq, c.ell, 1.0, x_o, c.logp, 5, 2, seq)
+    na = out["n_accept"].cpu().numpy()
+    np.testing.assert_array_equal(na, ref["n_accept"])
+    np.testing.assert_array_equal(out["next_token"].cpu().numpy(), ref["next_token"])
+    _rel_close(out["accept_mass"].cpu().numpy(), ref["beta"])
+    _rel_close(out["al_expected"].cpu().numpy(), ref["al"])
+    _rel_close(out["exp_len"].cpu().numpy(), ref["E"])
+    counts = ((na == 0).sum(), ((na > 0) & (na < K)).sum(), (na == K).sum())
+    print(f"[sample/verify] several chunks: reject at 0 / after accepts / full: {counts}", flush=True)
+    assert all(n > 0 for n in counts), counts
+
+
 @pytest.mark.parametrize("R,K", [(8, 8), (16, 6), (4, 8)])
 def test_accept_paths_at_the_benchmark_variants(R, K):
     """R = 8 / 16 / 4 (the specialisations the Qwen3, objective and stress workloads run):
