@@ -54,7 +54,7 @@ dbl_status check_aligned(std::initializer_list<std::pair<const void*, const char
 
 struct WsLayout {
   size_t total = 0;
-  size_t off[5] = {0, 0, 0, 0, 0};
+  size_t off[4] = {0, 0, 0, 0};
 };
 
 WsLayout layout(int op, const dbl_shape& s) {
@@ -63,7 +63,7 @@ WsLayout layout(int op, const dbl_shape& s) {
   const size_t R = static_cast<size_t>(s.R);
   const size_t nT = static_cast<size_t>(ntiles(s.V));
   const size_t nchunk = static_cast<size_t>(dbl::n_chunks(static_cast<int>(nT)));
-  size_t sizes[5] = {0, 0, 0, 0, 0};
+  size_t sizes[4] = {0, 0, 0, 0};
   int n = 0;
   switch (op) {
     case DBL_OP_HEAD:  // argmax keys, used only when argmax is requested
@@ -91,14 +91,12 @@ WsLayout layout(int op, const dbl_shape& s) {
       sizes[1] = B * K * nchunk * sizeof(float);
       sizes[2] = B * nT * sizeof(uint64_t);
       sizes[3] = B * nT * sizeof(uint64_t);
-      sizes[4] = B * sizeof(uint32_t);  // per-block arrival counters
-      n = 5;
+      n = 4;
       break;
     case DBL_OP_EXPECTED_LEN:
       sizes[0] = B * K * R * sizeof(double);
       sizes[1] = B * K * nchunk * sizeof(float);
-      sizes[2] = B * sizeof(uint32_t);  // per-block arrival counters
-      n = 3;
+      n = 2;
       break;
     case DBL_OP_TARGET:  // rows B*K: per-segment candidate lists and their counts
       sizes[0] = B * K * dbl::kFilterSegs * dbl::kFilterSegCap * sizeof(uint64_t);
@@ -219,7 +217,6 @@ dbl_status launch_verify_in(const dbl_shape& s, const float* tls, const float* l
   a.beta_part = reinterpret_cast<float*>(base + L.off[1]);
   a.res_tiles = reinterpret_cast<uint64_t*>(base + L.off[2]);
   a.p_tiles = reinterpret_cast<uint64_t*>(base + L.off[3]);
-  a.arrive = reinterpret_cast<uint32_t*>(base + L.off[4]);
   return hip_status(dbl::launch_verify(a, static_cast<hipStream_t>(stream)), "verify launch");
 }
 
@@ -401,7 +398,6 @@ dbl_status dbl_expected_len(dbl_shape s, const float* tls, const float* lmass,
   a.beta_part = reinterpret_cast<float*>(base + L.off[1]);
   a.res_tiles = nullptr;
   a.p_tiles = nullptr;
-  a.arrive = reinterpret_cast<uint32_t*>(base + L.off[2]);
   return hip_status(dbl::launch_verify(a, static_cast<hipStream_t>(stream)),
                     "expected_len launch");
 }

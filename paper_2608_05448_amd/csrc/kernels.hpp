@@ -57,7 +57,6 @@ struct VerifyArgs {
   float* beta_part;     // workspace [B*K, nchunk]
   uint64_t* res_tiles;  // workspace [B, nT]
   uint64_t* p_tiles;    // workspace [B, nT]
-  uint32_t* arrive;     // workspace [B]: stream workgroups of the block that have finished
 };
 
 // Greedy-branch mode: the branch tokens replace the branch log-probabilities (blk.tls, lmass and

@@ -14,11 +14,11 @@
 //             max(P - Q, 0) at the first rejected position (and of P for the fallback), or of
 //             the bonus row when every position was accepted.
 //   finalize  one 256-thread workgroup per block: acceptance masses,
-//             E = sum_i prod_{j<=i} beta_j, and the residual/bonus inverse-CDF draw.
-//   stream    (verification with V % 4 == 0 and masses requested: the usual case) beta,
-//             residual and finalize in one launch after the chain: the residual's tile sums come
-//             from the stream's own loads at the first rejected position, and the last of a
-//             block's workgroups to finish finalises it.
+//             E = sum_i prod_{j<=i} beta_j, and the residual/bonus inverse-CDF draw (the tile
+//             from the tile sums, then the tile's weights staged in LDS in one round of loads).
+//   stream    (verification with V % 4 == 0 and masses requested: the usual case) beta and
+//             residual in one launch between the chain and finalize: the residual's tile sums
+//             come from the stream's own loads at the first rejected position.
 // The expected-length reduction along a given trajectory runs chain, beta and finalize (no
 // accept test, no residual). Built with floating-point contraction off (determinism contract).
 #include <hip/hip_runtime.h>
@@ -39,7 +39,6 @@ __global__ __launch_bounds__(64) void chain_kernel(VerifyArgs a) {
   const BlockArgs& k_ = a.blk;
   const int64_t b = blockIdx.x;
   const int lane = lane_id();
-  if (a.arrive && lane == 0) a.arrive[b] = 0;  // read by the next launch's stream workgroups
   const int R = static_cast<int>(k_.R);
   const uint64_t seq = static_cast<uint64_t>(k_.seq_offset + b);
   double L = prior_log_weight(k_.prior + b * k_.R, R, k_.z_temp);
@@ -99,7 +98,6 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
   const int K = static_cast<int>(k_.K);
   const int KR = K * R;
   const uint64_t seq = static_cast<uint64_t>(k_.seq_offset + b);
-  if (a.arrive && tid == 0) a.arrive[b] = 0;  // read by the next launch's stream workgroups
   __shared__ float s_lq[kChainMaxKR];
   __shared__ double s_L[kChainMaxKR];
   __shared__ double s_L0[kMaxR];
@@ -280,32 +278,6 @@ __global__ __launch_bounds__(256) void beta_kernel(VerifyArgs a) {
   beta_body<RT>(a, blockIdx.x, blockIdx.y, gridDim.y);
 }
 
-// Integer weight of id v in the residual / bonus distributions.
-struct ResidualWeight {
-  const float* tls;
-  const float* lmass;
-  const float* lse;
-  const float* prow;   // target row at the position
-  int64_t m0;          // first branch row of the position
-  int64_t V;
-  int nT, R;
-  const double* w;     // posterior at the position (R values)
-  __device__ uint64_t p_int(int64_t v) const { return quant_detexp32(prow[v]); }
-  __device__ uint64_t q_int(int64_t v) const {
-    double Q = 0.0;
-    for (int z = 0; z < R; ++z) {
-      const int64_t m = m0 + z;
-      const float lq = flat_lq(tls[m * V + v], lmass[m * nT + v / kTile], lse[m]);
-      Q = __dadd_rn(Q, __dmul_rn(w[z], static_cast<double>(detexp32(lq))));
-    }
-    return quant40d(Q);
-  }
-  __device__ uint64_t res_int(int64_t v) const {
-    const uint64_t P = p_int(v), Q = q_int(v);
-    return P > Q ? P - Q : 0;
-  }
-};
-
 // Residual / bonus tile sums: workgroup (block, chunk of 32 vocabulary tiles), 8 lanes per
 // tile, each lane 16 ids read with 16-byte loads. At the first rejected position ks the integer
 // weights are P(v) = floor(detexp32(logp) 2^40) and R(v) = max(P(v) - Q(v), 0) with
@@ -449,10 +421,14 @@ __global__ __launch_bounds__(256) void beta_residual_kernel(VerifyArgs a) {
 
 // Block b: acceptance masses and E (binary64 sums of the chunk partials), then the residual or
 // bonus draw by inverse CDF over the tile sums. Run by a whole 256-thread workgroup.
+constexpr int kStageBatch = 8;  // loads in flight per thread when staging a tile's branch values
+
 __device__ void finalize_block(const VerifyArgs& a, int64_t b, int nchunk) {
   __shared__ double s_beta[kChainMaxK];
   __shared__ uint64_t lds[8];
   __shared__ double wz[kMaxR];
+  __shared__ uint64_t s_wt[kTile];         // integer weights of the selected tile
+  __shared__ float s_y[kMaxR * kTile];     // detexp32 of the tile's branch log-probabilities
   const BlockArgs& k_ = a.blk;
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -504,19 +480,56 @@ __device__ void finalize_block(const VerifyArgs& a, int64_t b, int nchunk) {
   const bool residual = ks < k_.K;
   int tok = -1;
   if (residual || a.Kp == k_.K + 1) {
-    if (residual && tid < k_.R) wz[tid] = a.wpost[(b * k_.K + ks) * k_.R + tid];
-    __syncthreads();
-    ResidualWeight W{k_.tls, k_.lmass, k_.lse, a.logp + (b * a.Kp + ks) * k_.V,
-                     (b * k_.K + (residual ? ks : 0)) * k_.R, k_.V, k_.nT,
-                     static_cast<int>(k_.R), wz};
+    const int64_t V = k_.V;
+    const int nT = k_.nT;
+    const int R = static_cast<int>(k_.R);
+    const float* prow = a.logp + (b * a.Kp + ks) * V;
+    const int64_t m0 = (b * k_.K + (residual ? ks : 0)) * k_.R;
     const uint32_t r = draw(k_.seed, kResidual, static_cast<uint32_t>(ks),
                             static_cast<uint64_t>(k_.seq_offset + b), k_.step);
-    if (residual)
-      tok = select_by_tiles_block(a.res_tiles + b * k_.nT, k_.nT, k_.V, r,
-                                  [&](int64_t v) { return W.res_int(v); }, lds);
-    if (tok < 0)
-      tok = select_by_tiles_block(a.p_tiles + b * k_.nT, k_.nT, k_.V, r,
-                                  [&](int64_t v) { return W.p_int(v); }, lds);
+    // The tile from the residual's tile sums, or from the target's when the residual has no
+    // mass (and for the bonus row).
+    Pick pk{-1, 0, 0};
+    if (residual) pk = pick_block(nT, [&](int t) { return a.res_tiles[b * nT + t]; }, r, lds);
+    const bool use_res = pk.i >= 0;
+    if (!use_res) pk = pick_block(nT, [&](int t) { return a.p_tiles[b * nT + t]; }, r, lds);
+    if (pk.i >= 0) {
+      // The tile's integer weights into LDS, with one round of loads by the whole workgroup:
+      // P(v), and for the residual the branch values detexp32(lq_z(v)) of every category.
+      const int64_t v0 = static_cast<int64_t>(pk.i) * kTile;
+      const int n = static_cast<int>(V - v0 < kTile ? V - v0 : kTile);
+      if (tid < n) s_wt[tid] = quant_detexp32(prow[v0 + tid]);
+      if (use_res) {
+        if (tid < R) wz[tid] = a.wpost[m0 + tid];
+        for (int base = 0; base < R * kTile; base += kStageBatch * 256) {
+          float lq[kStageBatch];
+#pragma unroll
+          for (int j = 0; j < kStageBatch; ++j) {  // clamped indices: every load is in bounds
+            const int idx = min(base + tid + 256 * j, R * kTile - 1);
+            const int64_t m = m0 + (idx >> 7);
+            const int i = min(idx & (kTile - 1), n - 1);
+            lq[j] = flat_lq(k_.tls[m * V + v0 + i], k_.lmass[m * nT + pk.i], k_.lse[m]);
+          }
+#pragma unroll
+          for (int j = 0; j < kStageBatch; ++j) {
+            const int idx = base + tid + 256 * j;
+            if (idx < R * kTile) s_y[idx] = detexp32(lq[j]);
+          }
+        }
+      }
+      __syncthreads();
+      if (use_res && tid < n) {
+        // R(v) = max(P(v) - Q(v), 0), Q(v) = floor((sum over ascending z of
+        // w_z detexp32(lq_z(v))) 2^40): the weights the residual's tile sums were taken from.
+        double Q = 0.0;
+        for (int z = 0; z < R; ++z)
+          Q = __dadd_rn(Q, __dmul_rn(wz[z], static_cast<double>(s_y[z * kTile + tid])));
+        const uint64_t P = s_wt[tid], Qi = quant40d(Q);
+        s_wt[tid] = P > Qi ? P - Qi : 0;
+      }
+      __syncthreads();
+      tok = pick_in_tile(s_wt, n, pk, lds);
+    }
   }
   if (tid == 0) a.next_token[b] = tok;
 }
@@ -525,18 +538,20 @@ __global__ __launch_bounds__(256) void finalize_kernel(VerifyArgs a, int nchunk)
   finalize_block(a, blockIdx.x, nchunk);
 }
 
-// The acceptance-mass stream with the residual tile sums and the per-block finalisation folded
-// in (V % 4 == 0, masses requested). Workgroup g handles chunk c = g % nchunk (32 vocabulary
-// tiles) of position row k of block b, g / nchunk = k B + b:
+// The acceptance-mass stream with the residual tile sums folded in (V % 4 == 0, masses
+// requested). Workgroup g handles chunk c = g % nchunk (32 vocabulary tiles; cpw consecutive
+// chunks at R <= 4) of position row k of block b, g / nchunk = k B + b:
 //  * k < K: the R branch rows and the target row of the chunk are read once for the
 //    acceptance-mass partial; at the block's first rejected position the same loaded values also
 //    give the contract's integer residual and target tile sums (weights as in residual_body), so
 //    no row is read twice;
 //  * k = K (rows of the bonus row, present when Kp = K + 1): read only when the block accepted
 //    every position, for the bonus row's integer tile sums.
-// Each workgroup then counts itself in its block's arrival counter (zeroed by the chain kernel
-// that precedes this launch); the last to arrive sees every partial of the block and finalises
-// it. Counting replaces the separate finalize launch; nothing waits on another workgroup.
+// The finalize launch that follows reduces the partials and draws. Finalising in the last of a
+// block's workgroups to finish instead (a per-block arrival counter after device-coherent
+// partial stores) measured slower: every workgroup held its slot through the store
+// acknowledgement and the counter's round trip (Qwen3-8B verification call 0.2339 ms with the
+// separate launch against 0.2504 ms).
 constexpr float kLog2eChunk = 1.4426950408889634f;
 
 // Eight waves per SIMD (64 VGPRs) up to eight categories: the binary64 residual arithmetic, which
@@ -556,7 +571,7 @@ __host__ __device__ constexpr bool stream_multi_chunk(int rt) { return rt > 0 &&
 
 template <int RT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(stream_waves<RT>(), 8)))
-void verify_stream_kernel(VerifyArgs a, int nchunk, int rows, int cpw) {
+void verify_stream_kernel(VerifyArgs a, int nchunk, int cpw) {
   const int CPW = stream_multi_chunk(RT) ? cpw : 1;
   const BlockArgs& k_ = a.blk;
   const int64_t B = k_.B;
@@ -571,7 +586,6 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows, int cpw) {
   __shared__ double s_wz[kMaxR];
   __shared__ float s_offx[kMaxR][kTilesPerChunk];  // fl32(lmass - lse) of the chunk's tiles
   __shared__ float red[4];
-  __shared__ int s_last;
   const int ks = a.trajectory ? -1 : a.n_accept[b];  // first rejected position, K if none
   const bool bonus = k == k_.K;
   const bool res = !a.trajectory && (bonus ? ks == k_.K : k == ks);
@@ -680,11 +694,8 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows, int cpw) {
           sr += __shfl_xor(sr, o);
         }
         if ((tid & 31) == 0 && tt < nt) {
-          __hip_atomic_store(a.p_tiles + b * k_.nT + t0 + tt, sp, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-          if (!bonus)
-            __hip_atomic_store(a.res_tiles + b * k_.nT + t0 + tt, sr, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+          a.p_tiles[b * k_.nT + t0 + tt] = sp;
+          if (!bonus) a.res_tiles[b * k_.nT + t0 + tt] = sr;
         }
       }
     }
@@ -694,24 +705,9 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int rows, int cpw) {
     if ((tid & 63) == 0) red[tid >> 6] = acc;
     __syncthreads();
     if (tid == 0)
-      __hip_atomic_store(a.beta_part + (b * k_.K + k) * nchunk + c,
-                         (red[0] + red[1]) + (red[2] + red[3]), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+      a.beta_part[(b * k_.K + k) * nchunk + c] = (red[0] + red[1]) + (red[2] + red[3]);
   }
   }
-  // Arrival. The partials above are device-coherent stores (written through the XCD's L2); each
-  // wave waits until its own have completed before the count is taken, so a workgroup that
-  // sees the final count sees every partial of the block once it has dropped its cached lines
-  // (one acquire in the last workgroup, instead of an L2 write-back in every workgroup).
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (tid == 0)
-    s_last = __hip_atomic_fetch_add(a.arrive + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-             static_cast<uint32_t>(rows) * ncw - 1u;
-  __syncthreads();
-  if (!s_last) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  finalize_block(a, b, nchunk);
 }
 
 }  // namespace
@@ -729,10 +725,11 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const bool want_beta = a.beta || a.exp_len;
-  if (want_beta && a.arrive && (a.blk.V & 3) == 0 && !a.trajectory) {
-    // One launch: stream, residual tile sums at the first rejection, finalisation. Trajectory
-    // mode keeps the two launches below: its stream kernel has no residual arithmetic to carry,
-    // and at R = 16 it measured 3.48 ms against 3.78 ms fused per 128-block chunk.
+  if (want_beta && (a.blk.V & 3) == 0 && !a.trajectory) {
+    // One stream: acceptance masses, and the residual tile sums at the first rejection from the
+    // same loads. Trajectory mode keeps the beta kernel below: its stream has no residual
+    // arithmetic to carry, and at R = 16 it measured 3.48 ms against 3.78 ms fused per 128-block
+    // chunk.
     const int rows = static_cast<int>(a.blk.K) + (!a.trajectory && a.Kp == a.blk.K + 1 ? 1 : 0);
     const int64_t R = a.blk.R;  // the template argument of the launch below: R, or 0
     const int rt = R == 1 || R == 2 || R == 4 || R == 8 || R == 16 ? static_cast<int>(R) : 0;
@@ -743,16 +740,15 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
     if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nwg));
     switch (a.blk.R) {
-      case 1: hipLaunchKernelGGL(verify_stream_kernel<1>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
-      case 2: hipLaunchKernelGGL(verify_stream_kernel<2>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
-      case 4: hipLaunchKernelGGL(verify_stream_kernel<4>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
-      case 8: hipLaunchKernelGGL(verify_stream_kernel<8>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
-      case 16: hipLaunchKernelGGL(verify_stream_kernel<16>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
-      default: hipLaunchKernelGGL(verify_stream_kernel<0>, grid, dim3(256), 0, stream, a, nchunk, rows, cpw); break;
+      case 1: hipLaunchKernelGGL(verify_stream_kernel<1>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
+      case 2: hipLaunchKernelGGL(verify_stream_kernel<2>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
+      case 4: hipLaunchKernelGGL(verify_stream_kernel<4>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
+      case 8: hipLaunchKernelGGL(verify_stream_kernel<8>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
+      case 16: hipLaunchKernelGGL(verify_stream_kernel<16>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
+      default: hipLaunchKernelGGL(verify_stream_kernel<0>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
     }
-    return hipGetLastError();
-  }
-  if (want_beta && !a.trajectory) {
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else if (want_beta && !a.trajectory) {
     if (npos + B > 0x7fffffff) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(B + npos), nchunk);
     switch (a.blk.R) {

@@ -185,19 +185,42 @@ __device__ __forceinline__ int select_by_tiles(const uint64_t* tiles, int nT, in
   return static_cast<int>(static_cast<int64_t>(tsel) * kTile + 2 * l + (pick0 ? 0 : 1));
 }
 
-// The same inverse-CDF selection done by a whole 256-thread workgroup (every thread calls it):
-// each thread sums a contiguous run of tile sums, a workgroup scan locates the run and then the
-// tile holding the threshold, and wavefront 0 scans that tile. `lds` must hold 8 uint64.
+// Workgroup inverse CDF over n integer weights weight(0..n-1) (every thread of a 256-thread
+// workgroup calls it, with the same n and r): each thread sums a contiguous run, a workgroup scan
+// gives the total Z and the run holding T = floor(r Z / 2^32), and that run's thread finds the
+// smallest index whose inclusive cumulative weight exceeds T. Runs of up to kRunRegs weights
+// (n <= 2048) are held in registers, their loads issued together with in-bounds (clamped)
+// indices, so the search costs one round of loads; longer runs are walked twice. Returns the
+// index (-1 when Z = 0) with T and the cumulative weight before it. `lds` must hold 8 uint64.
+struct Pick {
+  int i;
+  uint64_t T, before;
+};
+constexpr int kRunRegs = 8;
+
 template <class WeightFn>
-__device__ int select_by_tiles_block(const uint64_t* tiles, int nT, int64_t V, uint32_t r,
-                                     WeightFn weight, uint64_t* lds) {
+__device__ Pick pick_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
-  const int per = (nT + 255) / 256;
-  const int t0 = min(nT, tid * per), t1 = min(nT, t0 + per);
+  if (n <= 0) return Pick{-1, 0, 0};
+  const int per = (n + 255) / 256;
+  const int i0 = min(n, tid * per), i1 = min(n, i0 + per);
+  const bool regs = per <= kRunRegs;  // workgroup-uniform
+  uint64_t wr[kRunRegs];
   uint64_t part = 0;
-  for (int t = t0; t < t1; ++t) part += tiles[t];
+  if (regs) {
+    const int last = (i1 > i0 ? i1 : n) - 1;  // a valid index for the clamped loads
+#pragma unroll
+    for (int j = 0; j < kRunRegs; ++j) wr[j] = weight(min(i0 + j, last));
+#pragma unroll
+    for (int j = 0; j < kRunRegs; ++j) {
+      if (i0 + j >= i1) wr[j] = 0;
+      part += wr[j];
+    }
+  } else {
+    for (int i = i0; i < i1; ++i) part += weight(i);
+  }
   uint64_t incl = wave_incl_scan_u64(part);
   if (lane == 63) lds[wave] = incl;
   __syncthreads();
@@ -208,35 +231,66 @@ __device__ int select_by_tiles_block(const uint64_t* tiles, int nT, int64_t V, u
     Z += lds[w];
   }
   __syncthreads();
-  if (Z == 0) return -1;
+  if (Z == 0) return Pick{-1, 0, 0};
   const uint64_t T = icdf_threshold(r, Z);
   incl += base;
   const uint64_t excl = incl - part;
   if (excl <= T && T < incl) {  // exactly one thread's run holds the threshold
     uint64_t c = excl;
-    for (int t = t0; t < t1; ++t) {
-      if (c + tiles[t] > T) {
-        lds[4] = static_cast<uint64_t>(t);
-        lds[5] = c;
-        break;
+    if (regs) {
+      int found = -1;
+      uint64_t cb = 0;
+#pragma unroll
+      for (int j = 0; j < kRunRegs; ++j) {
+        if (found < 0 && c + wr[j] > T) {  // the run's total exceeds T: the first hit is in it
+          found = i0 + j;
+          cb = c;
+        }
+        c += wr[j];
       }
-      c += tiles[t];
+      lds[4] = static_cast<uint64_t>(found);
+      lds[5] = cb;
+    } else {
+      for (int i = i0; i < i1; ++i) {
+        const uint64_t wi = weight(i);
+        if (c + wi > T) {
+          lds[4] = static_cast<uint64_t>(i);
+          lds[5] = c;
+          break;
+        }
+        c += wi;
+      }
     }
   }
   __syncthreads();
-  const int tsel = static_cast<int>(lds[4]);
-  const uint64_t before = lds[5];
-  if (wave == 0) {
-    const int64_t v0 = static_cast<int64_t>(tsel) * kTile + 2 * lane;
-    const uint64_t q0 = v0 < V ? weight(v0) : 0;
-    const uint64_t q1 = v0 + 1 < V ? weight(v0 + 1) : 0;
+  const Pick pk{static_cast<int>(lds[4]), T, lds[5]};
+  __syncthreads();
+  return pk;
+}
+
+// The selection of pick_block, index only.
+template <class WeightFn>
+__device__ int select_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
+  return pick_block(n, weight, r, lds).i;
+}
+
+// In-tile step of a two-level inverse CDF: wavefront 0 scans the n <= 128 integer weights w[i]
+// of tile pk.i (ids 128 pk.i + i, held in LDS), two per lane, and returns to every thread the
+// smallest id whose cumulative weight after pk.before exceeds pk.T (-1 if none: unreachable when
+// the tile sums are those of the weights). `lds` must hold 8 uint64.
+__device__ __forceinline__ int pick_in_tile(const uint64_t* w, int n, const Pick& pk,
+                                            uint64_t* lds) {
+  if (threadIdx.x < 64) {
+    const int lane = lane_id();
+    const uint64_t q0 = 2 * lane < n ? w[2 * lane] : 0;
+    const uint64_t q1 = 2 * lane + 1 < n ? w[2 * lane + 1] : 0;
     const uint64_t in = wave_incl_scan_u64(q0 + q1);
-    const bool h0 = before + in - q1 > T, h1 = before + in > T;
+    const bool h0 = pk.before + in - q1 > pk.T, h1 = pk.before + in > pk.T;
     const uint64_t hit = __ballot(h0 || h1);
     const int l = hit ? __ffsll(static_cast<unsigned long long>(hit)) - 1 : 0;
     const int pick0 = __shfl(static_cast<int>(h0), l);  // whole wavefront active
     if (lane == 0)
-      lds[6] = hit ? static_cast<uint64_t>(static_cast<int64_t>(tsel) * kTile + 2 * l +
+      lds[6] = hit ? static_cast<uint64_t>(static_cast<int64_t>(pk.i) * kTile + 2 * l +
                                            (pick0 ? 0 : 1))
                    : ~0ull;
   }
@@ -246,49 +300,24 @@ __device__ int select_by_tiles_block(const uint64_t* tiles, int nT, int64_t V, u
   return res == ~0ull ? -1 : static_cast<int>(res);
 }
 
-// Inverse CDF over n integer weights weight(0..n-1) by a 256-thread workgroup (every thread
-// calls it, with the same n and r): each thread sums a contiguous run, a workgroup scan gives
-// the total Z and the run holding the threshold T = floor(r Z / 2^32), and that run's thread
-// finds the smallest index whose inclusive cumulative weight exceeds T. Returns -1 when Z = 0.
-// `lds` must hold 8 uint64; weight(i) is called twice for the indices of the selected run.
+// Two-level inverse CDF over per-tile integer sums by a whole 256-thread workgroup (every thread
+// calls it): pick_block finds the tile holding the threshold, then wavefront 0 evaluates
+// weight(v) for the tile's ids (v < V) into LDS and scans them.
 template <class WeightFn>
-__device__ int select_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
-  const int tid = threadIdx.x;
-  const int lane = lane_id();
-  const int wave = tid >> 6;
-  const int per = (n + 255) / 256;
-  const int i0 = min(n, tid * per), i1 = min(n, i0 + per);
-  uint64_t part = 0;
-  for (int i = i0; i < i1; ++i) part += weight(i);
-  uint64_t incl = wave_incl_scan_u64(part);
-  if (lane == 63) lds[wave] = incl;
-  __syncthreads();
-  uint64_t base = 0, Z = 0;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    if (w < wave) base += lds[w];
-    Z += lds[w];
+__device__ int select_by_tiles_block(const uint64_t* tiles, int nT, int64_t V, uint32_t r,
+                                     WeightFn weight, uint64_t* lds) {
+  __shared__ uint64_t s_wt[kTile];
+  const Pick pk = pick_block(nT, [&](int t) { return tiles[t]; }, r, lds);
+  if (pk.i < 0) return -1;
+  const int64_t v0 = static_cast<int64_t>(pk.i) * kTile;
+  const int n = static_cast<int>(V - v0 < kTile ? V - v0 : kTile);
+  if (threadIdx.x < 64) {
+    const int lane = lane_id();
+    if (2 * lane < n) s_wt[2 * lane] = weight(v0 + 2 * lane);
+    if (2 * lane + 1 < n) s_wt[2 * lane + 1] = weight(v0 + 2 * lane + 1);
   }
   __syncthreads();
-  if (Z == 0) return -1;
-  const uint64_t T = icdf_threshold(r, Z);
-  incl += base;
-  const uint64_t excl = incl - part;
-  if (excl <= T && T < incl) {  // exactly one thread's run holds the threshold
-    uint64_t c = excl;
-    for (int i = i0; i < i1; ++i) {
-      const uint64_t wi = weight(i);
-      if (c + wi > T) {
-        lds[4] = static_cast<uint64_t>(i);
-        break;
-      }
-      c += wi;
-    }
-  }
-  __syncthreads();
-  const int res = static_cast<int>(lds[4]);
-  __syncthreads();
-  return res;
+  return pick_in_tile(s_wt, n, pk, lds);
 }
 
 }  // namespace dbl
