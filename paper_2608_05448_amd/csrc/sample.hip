@@ -41,12 +41,14 @@ __global__ __launch_bounds__(256) void sample_kernel(SampleArgs a) {
     const PhiloxPair r = draw2(k_.seed, kToken, static_cast<uint32_t>(k),
                                static_cast<uint64_t>(k_.seq_offset + b), k_.step);
     const int t = select_block(
-        k_.nT, [&](int i) { return quant_detexp32(__fsub_rn(lm[i], lse)); }, r.w0, lds);
+        k_.nT, [&](int i) { return lm[i]; },
+        [&](float l) { return quant_detexp32(__fsub_rn(l, lse)); }, r.w0, lds);
     if (t >= 0) {
       const int64_t v0 = static_cast<int64_t>(t) * kTile;
       const int n = static_cast<int>(k_.V - v0 < kTile ? k_.V - v0 : kTile);
       const float* tile = k_.tls + m * k_.V + v0;
-      const int j = select_block(n, [&](int i) { return quant_detexp32(tile[i]); }, r.w1, lds);
+      const int j = select_block(
+          n, [&](int i) { return tile[i]; }, [](float v) { return quant_detexp32(v); }, r.w1, lds);
       if (j >= 0) x = static_cast<int>(v0 + j);
     }
   }

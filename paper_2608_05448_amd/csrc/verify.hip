@@ -103,31 +103,59 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
   __shared__ double s_L0[kMaxR];
   __shared__ double s_Q[kChainMaxK];
   __shared__ double s_P[kChainMaxK];
-  if (wave == 0) {
-    const double l0 = prior_log_weight(k_.prior + b * k_.R, R, k_.z_temp);
-    if (lane < R) s_L0[lane] = l0;
-  }
-  for (int i = tid; i < KR; i += blockDim.x) {
-    const int k = i / R, z = i % R;
-    const int64_t row = (b * k_.K + k) * k_.R + z;
-    const int32_t xk = a.x[b * k_.K + k];
-    s_lq[i] = in_vocab(xk, k_.V)
-                  ? flat_lq(k_.tls[row * k_.V + xk], k_.lmass[row * k_.nT + xk / kTile], k_.lse[row])
-                  : -INFINITY;
-  }
-  if (!a.trajectory) {
-    for (int k = tid; k < K; k += blockDim.x) {
+  if (KR <= static_cast<int>(blockDim.x)) {
+    // At most one (k, z) per thread (every workload shape of the paper): the drafted tokens and
+    // the prior, then the branch and target values at the tokens, each round of loads issued
+    // together with clamped (in-bounds) indices before any value is used.
+    const int i = min(tid, KR - 1), k = i / R, z = i % R, kp = min(tid, K - 1);
+    const int32_t xk = a.x[b * k_.K + k], xp = a.x[b * k_.K + kp];
+    const float pl = k_.prior[b * k_.R + min(lane, R - 1)];
+    const bool okq = in_vocab(xk, k_.V), okp = in_vocab(xp, k_.V);
+    const int64_t row = (b * k_.K + k) * k_.R + z, vq = okq ? xk : 0, vp = okp ? xp : 0;
+    const float t = k_.tls[row * k_.V + vq], lm = k_.lmass[row * k_.nT + vq / kTile];
+    const float ls = k_.lse[row], lp = a.logp[(b * a.Kp + kp) * k_.V + vp];
+    if (wave == 0) {
+      const double l0 = prior_log_weight_of(pl, R, k_.z_temp);
+      if (lane < R) s_L0[lane] = l0;
+    }
+    if (tid < KR) s_lq[tid] = okq ? flat_lq(t, lm, ls) : -INFINITY;
+    if (!a.trajectory && tid < K) s_P[tid] = okp ? static_cast<double>(detexp32(lp)) : 0.0;
+  } else {
+    if (wave == 0) {
+      const double l0 = prior_log_weight(k_.prior + b * k_.R, R, k_.z_temp);
+      if (lane < R) s_L0[lane] = l0;
+    }
+    for (int i = tid; i < KR; i += blockDim.x) {
+      const int k = i / R, z = i % R;
+      const int64_t row = (b * k_.K + k) * k_.R + z;
       const int32_t xk = a.x[b * k_.K + k];
-      s_P[k] = in_vocab(xk, k_.V)
-                   ? static_cast<double>(detexp32(a.logp[(b * a.Kp + k) * k_.V + xk]))
-                   : 0.0;
+      s_lq[i] = in_vocab(xk, k_.V) ? flat_lq(k_.tls[row * k_.V + xk],
+                                             k_.lmass[row * k_.nT + xk / kTile], k_.lse[row])
+                                   : -INFINITY;
+    }
+    if (!a.trajectory) {
+      for (int k = tid; k < K; k += blockDim.x) {
+        const int32_t xk = a.x[b * k_.K + k];
+        s_P[k] = in_vocab(xk, k_.V)
+                     ? static_cast<double>(detexp32(a.logp[(b * a.Kp + k) * k_.V + xk]))
+                     : 0.0;
+      }
     }
   }
   __syncthreads();
   for (int i = tid; i < KR; i += blockDim.x) {
     const int k = i / R, z = i % R;
     double L = s_L0[z];
-    for (int j = 0; j < k; ++j) L = __dadd_rn(L, static_cast<double>(s_lq[j * R + z]));
+    int j = 0;
+    for (; j + 4 <= k; j += 4) {  // four LDS reads in flight; the additions stay in order
+      const float q0 = s_lq[j * R + z], q1 = s_lq[(j + 1) * R + z];
+      const float q2 = s_lq[(j + 2) * R + z], q3 = s_lq[(j + 3) * R + z];
+      L = __dadd_rn(L, static_cast<double>(q0));
+      L = __dadd_rn(L, static_cast<double>(q1));
+      L = __dadd_rn(L, static_cast<double>(q2));
+      L = __dadd_rn(L, static_cast<double>(q3));
+    }
+    for (; j < k; ++j) L = __dadd_rn(L, static_cast<double>(s_lq[j * R + z]));
     s_L[i] = L;
   }
   __syncthreads();
@@ -434,20 +462,27 @@ __device__ void finalize_block(const VerifyArgs& a, int64_t b, int nchunk) {
   const int lane = lane_id();
   const int wave = tid >> 6;
   const int K = static_cast<int>(k_.K);
+  __shared__ int s_ks;
+  // The first rejected position, loaded together with the partials below (an LDS copy keeps the
+  // load ahead of the reduction's barriers).
+  if (!a.trajectory && tid == 0) s_ks = a.n_accept[b];
   if (a.beta || a.exp_len) {
     for (int k0 = 0; k0 < K; k0 += kChainMaxK) {
       const int kn = min(kChainMaxK, K - k0);
-      // Four positions per wavefront at a time: their loads and reductions overlap (each
-      // position's sum is taken in the same order as one at a time).
+      // Four positions per wavefront at a time, their loads issued together with clamped
+      // (in-bounds) indices before any is summed; each position's sum is taken in the same order
+      // as one at a time: lane l adds chunks l, l + 64, ..., then a wavefront sum.
       for (int kk0 = 4 * wave; kk0 < kn; kk0 += 16) {
-        double sum[4];
+        double sum[4] = {0.0, 0.0, 0.0, 0.0};
+        for (int c0 = 0; c0 < nchunk; c0 += 64) {  // one pass up to 64 chunks
+          const int c = min(c0 + lane, nchunk - 1);
+          float v[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          sum[u] = 0.0;
-          if (kk0 + u < kn) {
-            const float* part = a.beta_part + (b * k_.K + k0 + kk0 + u) * nchunk;
-            for (int c = lane; c < nchunk; c += 64) sum[u] += static_cast<double>(part[c]);
-          }
+          for (int u = 0; u < 4; ++u)
+            v[u] = a.beta_part[(b * k_.K + k0 + min(kk0 + u, kn - 1)) * nchunk + c];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (c0 + lane < nchunk) sum[u] += static_cast<double>(v[u]);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) sum[u] = wave_sum_f64(sum[u]);
@@ -476,7 +511,8 @@ __device__ void finalize_block(const VerifyArgs& a, int64_t b, int nchunk) {
     }
   }
   if (a.trajectory) return;
-  const int ks = a.n_accept[b];
+  __syncthreads();
+  const int ks = s_ks;
   const bool residual = ks < k_.K;
   int tok = -1;
   if (residual || a.Kp == k_.K + 1) {
@@ -490,33 +526,40 @@ __device__ void finalize_block(const VerifyArgs& a, int64_t b, int nchunk) {
     // The tile from the residual's tile sums, or from the target's when the residual has no
     // mass (and for the bonus row).
     Pick pk{-1, 0, 0};
-    if (residual) pk = pick_block(nT, [&](int t) { return a.res_tiles[b * nT + t]; }, r, lds);
+    if (residual)
+      pk = pick_block(nT, [&](int t) { return a.res_tiles[b * nT + t]; }, weigh_u64, r, lds);
     const bool use_res = pk.i >= 0;
-    if (!use_res) pk = pick_block(nT, [&](int t) { return a.p_tiles[b * nT + t]; }, r, lds);
+    if (!use_res)
+      pk = pick_block(nT, [&](int t) { return a.p_tiles[b * nT + t]; }, weigh_u64, r, lds);
     if (pk.i >= 0) {
       // The tile's integer weights into LDS, with one round of loads by the whole workgroup:
       // P(v), and for the residual the branch values detexp32(lq_z(v)) of every category.
       const int64_t v0 = static_cast<int64_t>(pk.i) * kTile;
       const int n = static_cast<int>(V - v0 < kTile ? V - v0 : kTile);
-      if (tid < n) s_wt[tid] = quant_detexp32(prow[v0 + tid]);
-      if (use_res) {
-        if (tid < R) wz[tid] = a.wpost[m0 + tid];
-        for (int base = 0; base < R * kTile; base += kStageBatch * 256) {
-          float lq[kStageBatch];
+      const float pv = prow[v0 + min(tid, n - 1)];  // raw values first, clamped indices
+      const double wv = a.wpost[m0 + min(tid, R - 1)];
+      auto stage = [&](int base) {  // kStageBatch branch values per thread, loads first
+        float lq[kStageBatch];
 #pragma unroll
-          for (int j = 0; j < kStageBatch; ++j) {  // clamped indices: every load is in bounds
-            const int idx = min(base + tid + 256 * j, R * kTile - 1);
-            const int64_t m = m0 + (idx >> 7);
-            const int i = min(idx & (kTile - 1), n - 1);
-            lq[j] = flat_lq(k_.tls[m * V + v0 + i], k_.lmass[m * nT + pk.i], k_.lse[m]);
-          }
-#pragma unroll
-          for (int j = 0; j < kStageBatch; ++j) {
-            const int idx = base + tid + 256 * j;
-            if (idx < R * kTile) s_y[idx] = detexp32(lq[j]);
-          }
+        for (int j = 0; j < kStageBatch; ++j) {  // clamped indices: every load is in bounds
+          const int idx = min(base + tid + 256 * j, R * kTile - 1);
+          const int64_t m = m0 + (idx >> 7);
+          const int i = min(idx & (kTile - 1), n - 1);
+          lq[j] = flat_lq(k_.tls[m * V + v0 + i], k_.lmass[m * nT + pk.i], k_.lse[m]);
         }
+#pragma unroll
+        for (int j = 0; j < kStageBatch; ++j) {
+          const int idx = base + tid + 256 * j;
+          if (idx < R * kTile) s_y[idx] = detexp32(lq[j]);
+        }
+      };
+      if (use_res) {
+        stage(0);  // R <= 16: straight-line, in flight with the two loads above
+        for (int base = kStageBatch * 256; base < R * kTile; base += kStageBatch * 256)
+          stage(base);
       }
+      if (tid < n) s_wt[tid] = quant_detexp32(pv);
+      if (use_res && tid < R) wz[tid] = wv;
       __syncthreads();
       if (use_res && tid < n) {
         // R(v) = max(P(v) - Q(v), 0), Q(v) = floor((sum over ascending z of

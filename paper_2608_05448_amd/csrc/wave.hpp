@@ -77,11 +77,12 @@ __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
   return v;
 }
 
-// Unnormalised log prior of category z = lane (lanes >= R hold -inf): l_z / Z_T, or for
-// Z_T = 0, 0 at the lowest-index maximum of l and -inf elsewhere.
-__device__ __forceinline__ double prior_log_weight(const float* prior_row, int R, float z_temp) {
+// Unnormalised log prior of category z = lane (lanes >= R hold -inf) from raw = l_lane (any
+// value on lanes >= R): l_z / Z_T, or for Z_T = 0, 0 at the lowest-index maximum of l and -inf
+// elsewhere.
+__device__ __forceinline__ double prior_log_weight_of(float raw, int R, float z_temp) {
   const int lane = lane_id();
-  const float l = lane < R ? prior_row[lane] : -INFINITY;
+  const float l = lane < R ? raw : -INFINITY;
   if (z_temp > 0.0f)
     return lane < R ? static_cast<double>(l) / static_cast<double>(z_temp) : -INFINITY;
   float mx = l;
@@ -90,6 +91,11 @@ __device__ __forceinline__ double prior_log_weight(const float* prior_row, int R
   const uint64_t hit = __ballot(lane < R && l == mx);
   const int top = __ffsll(static_cast<unsigned long long>(hit)) - 1;
   return lane == top ? 0.0 : -INFINITY;
+}
+
+// The same, loading l from the block's prior row (clamped index: every lane's load is in bounds).
+__device__ __forceinline__ double prior_log_weight(const float* prior_row, int R, float z_temp) {
+  return prior_log_weight_of(prior_row[min(lane_id(), R - 1)], R, z_temp);
 }
 
 // w_z = exp(L_z - max L) / sum_z exp(L_z - max L), the sum taken over ascending z with each
@@ -185,21 +191,23 @@ __device__ __forceinline__ int select_by_tiles(const uint64_t* tiles, int nT, in
   return static_cast<int>(static_cast<int64_t>(tsel) * kTile + 2 * l + (pick0 ? 0 : 1));
 }
 
-// Workgroup inverse CDF over n integer weights weight(0..n-1) (every thread of a 256-thread
-// workgroup calls it, with the same n and r): each thread sums a contiguous run, a workgroup scan
-// gives the total Z and the run holding T = floor(r Z / 2^32), and that run's thread finds the
-// smallest index whose inclusive cumulative weight exceeds T. Runs of up to kRunRegs weights
-// (n <= 2048) are held in registers, their loads issued together with in-bounds (clamped)
-// indices, so the search costs one round of loads; longer runs are walked twice. Returns the
-// index (-1 when Z = 0) with T and the cumulative weight before it. `lds` must hold 8 uint64.
+// Workgroup inverse CDF over n integer weights weigh(load(i)), i < n (every thread of a
+// 256-thread workgroup calls it, with the same n and r): each thread sums a contiguous run, a
+// workgroup scan gives the total Z and the run holding T = floor(r Z / 2^32), and that run's
+// thread finds the smallest index whose inclusive cumulative weight exceeds T. Runs of up to
+// kRunRegs values (n <= 2048) are loaded into registers first, all with in-bounds (clamped)
+// indices, and weighed afterwards, so the loads are in flight together (a weight function with
+// branches would otherwise wait for each load in turn); longer runs are walked twice. Returns
+// the index (-1 when Z = 0) with T and the cumulative weight before it. `lds` must hold 8
+// uint64.
 struct Pick {
   int i;
   uint64_t T, before;
 };
 constexpr int kRunRegs = 8;
 
-template <class WeightFn>
-__device__ Pick pick_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
+template <class LoadFn, class WeighFn>
+__device__ Pick pick_block(int n, LoadFn load, WeighFn weigh, uint32_t r, uint64_t* lds) {
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
@@ -211,15 +219,16 @@ __device__ Pick pick_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
   uint64_t part = 0;
   if (regs) {
     const int last = (i1 > i0 ? i1 : n) - 1;  // a valid index for the clamped loads
+    decltype(load(0)) raw[kRunRegs];
 #pragma unroll
-    for (int j = 0; j < kRunRegs; ++j) wr[j] = weight(min(i0 + j, last));
+    for (int j = 0; j < kRunRegs; ++j) raw[j] = load(min(i0 + j, last));
 #pragma unroll
     for (int j = 0; j < kRunRegs; ++j) {
-      if (i0 + j >= i1) wr[j] = 0;
+      wr[j] = i0 + j < i1 ? static_cast<uint64_t>(weigh(raw[j])) : 0;
       part += wr[j];
     }
   } else {
-    for (int i = i0; i < i1; ++i) part += weight(i);
+    for (int i = i0; i < i1; ++i) part += weigh(load(i));
   }
   uint64_t incl = wave_incl_scan_u64(part);
   if (lane == 63) lds[wave] = incl;
@@ -252,7 +261,7 @@ __device__ Pick pick_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
       lds[5] = cb;
     } else {
       for (int i = i0; i < i1; ++i) {
-        const uint64_t wi = weight(i);
+        const uint64_t wi = weigh(load(i));
         if (c + wi > T) {
           lds[4] = static_cast<uint64_t>(i);
           lds[5] = c;
@@ -269,10 +278,12 @@ __device__ Pick pick_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
 }
 
 // The selection of pick_block, index only.
-template <class WeightFn>
-__device__ int select_block(int n, WeightFn weight, uint32_t r, uint64_t* lds) {
-  return pick_block(n, weight, r, lds).i;
+template <class LoadFn, class WeighFn>
+__device__ int select_block(int n, LoadFn load, WeighFn weigh, uint32_t r, uint64_t* lds) {
+  return pick_block(n, load, weigh, r, lds).i;
 }
+
+__device__ __forceinline__ uint64_t weigh_u64(uint64_t w) { return w; }
 
 // In-tile step of a two-level inverse CDF: wavefront 0 scans the n <= 128 integer weights w[i]
 // of tile pk.i (ids 128 pk.i + i, held in LDS), two per lane, and returns to every thread the
@@ -307,7 +318,7 @@ template <class WeightFn>
 __device__ int select_by_tiles_block(const uint64_t* tiles, int nT, int64_t V, uint32_t r,
                                      WeightFn weight, uint64_t* lds) {
   __shared__ uint64_t s_wt[kTile];
-  const Pick pk = pick_block(nT, [&](int t) { return tiles[t]; }, r, lds);
+  const Pick pk = pick_block(nT, [&](int t) { return tiles[t]; }, weigh_u64, r, lds);
   if (pk.i < 0) return -1;
   const int64_t v0 = static_cast<int64_t>(pk.i) * kTile;
   const int n = static_cast<int>(V - v0 < kTile ? V - v0 : kTile);
