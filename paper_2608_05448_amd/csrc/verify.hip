@@ -103,7 +103,10 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
   __shared__ double s_L0[kMaxR];
   __shared__ double s_Q[kChainMaxK];
   __shared__ double s_P[kChainMaxK];
+  uint32_t r_first = 0;  // wavefront 0: the accept draw of position lane (K R <= 256)
+  bool have_r = false;
   if (KR <= static_cast<int>(blockDim.x)) {
+    have_r = true;
     // At most one (k, z) per thread (every workload shape of the paper): the drafted tokens and
     // the prior, then the branch and target values at the tokens, each round of loads issued
     // together with clamped (in-bounds) indices before any value is used.
@@ -114,6 +117,9 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
     const int64_t row = (b * k_.K + k) * k_.R + z, vq = okq ? xk : 0, vp = okp ? xp : 0;
     const float t = k_.tls[row * k_.V + vq], lm = k_.lmass[row * k_.nT + vq / kTile];
     const float ls = k_.lse[row], lp = a.logp[(b * a.Kp + kp) * k_.V + vp];
+    // Wavefront 0's accept draws for positions 0..63, computed while the loads are in flight.
+    if (wave == 0 && !a.trajectory)
+      r_first = draw(k_.seed, kAccept, static_cast<uint32_t>(lane), seq, k_.step);
     if (wave == 0) {
       const double l0 = prior_log_weight_of(pl, R, k_.z_temp);
       if (lane < R) s_L0[lane] = l0;
@@ -173,8 +179,20 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
       if (!a.trajectory) {
         const double y = own ? static_cast<double>(detexp32(s_lq[k * R + z])) : 0.0;
         double Q = 0.0;
-        for (int zz = 0; zz < R; ++zz)
-          Q = __dadd_rn(Q, __dmul_rn(__shfl(w, seg * G + zz), __shfl(y, seg * G + zz)));
+        if constexpr (G <= 16) {  // all shuffles in flight, then the ordered sum
+          double wv[G], yv[G];
+#pragma unroll
+          for (int zz = 0; zz < G; ++zz) {
+            wv[zz] = __shfl(w, seg * G + zz);
+            yv[zz] = __shfl(y, seg * G + zz);
+          }
+#pragma unroll
+          for (int zz = 0; zz < G; ++zz)
+            if (zz < R) Q = __dadd_rn(Q, __dmul_rn(wv[zz], yv[zz]));
+        } else {
+          for (int zz = 0; zz < R; ++zz)
+            Q = __dadd_rn(Q, __dmul_rn(__shfl(w, seg * G + zz), __shfl(y, seg * G + zz)));
+        }
         if (k < K && z == 0) s_Q[k] = Q;
       }
     }
@@ -202,7 +220,9 @@ __global__ __launch_bounds__(256) void chain_parallel_kernel(VerifyArgs a) {
       if (k < K) {
         const double Q = s_Q[k], P = s_P[k];
         A = Q > 0.0 ? fmin(1.0, P / Q) : (P > 0.0 ? 1.0 : 0.0);
-        const uint32_t r = draw(k_.seed, kAccept, static_cast<uint32_t>(k), seq, k_.step);
+        const uint32_t r = k0 == 0 && have_r
+                               ? r_first
+                               : draw(k_.seed, kAccept, static_cast<uint32_t>(k), seq, k_.step);
         rej = !accept_int(r, quant40d(Q), quant40d(P));
       }
       const uint64_t rejm = __ballot(rej);
@@ -495,17 +515,24 @@ __device__ void finalize_block(const VerifyArgs& a, int64_t b, int nchunk) {
       __syncthreads();
       for (int kk = tid; kk < kn; kk += blockDim.x)
         if (a.beta) a.beta[b * k_.K + k0 + kk] = static_cast<float>(s_beta[kk]);
-      if (a.exp_len && tid == 0) {
-        // Running product and sum over all positions; kept in lds[7] / lds[6] across chunks.
+      if (a.exp_len && wave == 0) {
+        // Running product and sum over all positions in order, kept in lds[7] / lds[6] across
+        // chunks; every lane of wavefront 0 takes the same steps on values held in its lanes.
         double prod = k0 == 0 ? 1.0 : __longlong_as_double(static_cast<long long>(lds[7]));
         double E = k0 == 0 ? 0.0 : __longlong_as_double(static_cast<long long>(lds[6]));
-        for (int kk = 0; kk < kn; ++kk) {
-          prod *= s_beta[kk];
-          E += prod;
+        for (int c0 = 0; c0 < kn; c0 += 64) {
+          const double bv = s_beta[min(c0 + lane, kn - 1)];
+          const int cn = min(64, kn - c0);
+          for (int j = 0; j < cn; ++j) {
+            prod *= lane_f64(bv, j);
+            E += prod;
+          }
         }
-        lds[7] = static_cast<uint64_t>(__double_as_longlong(prod));
-        lds[6] = static_cast<uint64_t>(__double_as_longlong(E));
-        if (k0 + kn == K) a.exp_len[b] = static_cast<float>(E);
+        if (lane == 0) {
+          lds[7] = static_cast<uint64_t>(__double_as_longlong(prod));
+          lds[6] = static_cast<uint64_t>(__double_as_longlong(E));
+          if (k0 + kn == K) a.exp_len[b] = static_cast<float>(E);
+        }
       }
       __syncthreads();
     }

@@ -114,16 +114,37 @@ __device__ __forceinline__ double normalize_weight(double L, int R) {
 // normalize_weight for several positions per wavefront: lanes in segments of G (a power of two,
 // R <= G <= 64), lane z of a segment holding category z's log weight. Each segment gets exactly
 // what normalize_weight gives a wavefront holding the same values (same operations, same order).
+// Up to 16 lanes per segment the segment's values are gathered with all shuffles in flight
+// before the ordered maximum and sum (fixed-count loops); wider segments walk them in turn.
 template <int G>
 __device__ __forceinline__ double normalize_weight_seg(double L, int R) {
   const int base = lane_id() & ~(G - 1);
-  double mx = __shfl(L, base);
-  for (int z = 1; z < R; ++z) mx = fmax(mx, __shfl(L, base + z));
-  if (!(mx > -INFINITY)) return 0.0;
-  const double e = dexp64(__dsub_rn(L, mx));
-  double S = 0.0;
-  for (int z = 0; z < R; ++z) S = __dadd_rn(S, __shfl(e, base + z));
-  return e / S;
+  if constexpr (G <= 16) {
+    double v[G];
+#pragma unroll
+    for (int z = 0; z < G; ++z) v[z] = __shfl(L, base + z);
+    double mx = v[0];
+#pragma unroll
+    for (int z = 1; z < G; ++z)
+      if (z < R) mx = fmax(mx, v[z]);
+    if (!(mx > -INFINITY)) return 0.0;
+    const double e = dexp64(__dsub_rn(L, mx));
+#pragma unroll
+    for (int z = 0; z < G; ++z) v[z] = __shfl(e, base + z);
+    double S = 0.0;
+#pragma unroll
+    for (int z = 0; z < G; ++z)
+      if (z < R) S = __dadd_rn(S, v[z]);
+    return e / S;
+  } else {
+    double mx = __shfl(L, base);
+    for (int z = 1; z < R; ++z) mx = fmax(mx, __shfl(L, base + z));
+    if (!(mx > -INFINITY)) return 0.0;
+    const double e = dexp64(__dsub_rn(L, mx));
+    double S = 0.0;
+    for (int z = 0; z < R; ++z) S = __dadd_rn(S, __shfl(e, base + z));
+    return e / S;
+  }
 }
 
 // The category z ~ q_{Z_T} of block b by inverse CDF on floor(w_z 2^40); all lanes agree.

@@ -39,9 +39,14 @@ CASES = [
     ("long-chain", 3, 100, 2, 500, 8, "aligned-block", 1, 1.0, 1.0, 14, 0, 0),
     # K > 256: sequential chain, and the finalize kernel carries E across position chunks.
     ("chunked-finalize", 2, 300, 1, 300, 8, "aligned-block", 1, 1.0, 1.0, 15, 1, 3),
+    # 256 < K R <= 2048: the parallel chain gathers in a loop; 17 <= R <= 32 normalises over
+    # 32-lane segments, R <= 16 over 8-lane segments.
+    ("looped-gather-r24", 4, 12, 24, 800, 16, "aligned-block", 1, 1.0, 1.0, 16, 0, 2),
+    ("looped-gather-r8", 16, 40, 8, 600, 16, "aligned-block", 1, 1.0, 1.0, 17, 4, 0),
 ]
 NOISE = {"bench-variant-r8": 0.1, "objective-variant-r16": 0.1, "r4-stress-variant": 0.1,
-         "long-chain": 0.02, "chunked-finalize": 0.02}
+         "long-chain": 0.02, "chunked-finalize": 0.02, "looped-gather-r24": 0.05,
+         "looped-gather-r8": 0.02}
 
 
 def _rel_close(got, want, rtol=1e-4, floor=1e-30):
