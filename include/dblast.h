@@ -63,8 +63,9 @@
  *    DBL_EINVAL.
  *  - Streams: work is enqueued on `stream` (a hipStream_t; NULL is the default stream) and the
  *    call returns without waiting. Outputs are valid once the stream reaches that point. No
- *    call allocates, frees, copies, sets memory or synchronises: workspaces are cleared by
- *    kernels, so the calls may be captured into a HIP graph and replayed.
+ *    call allocates, frees, copies, sets memory or synchronises, and no workspace needs clearing
+ *    (within a call, every workspace word is written before it is read), so the calls may be
+ *    captured into a HIP graph and replayed.
  *  - Errors: a non-zero dbl_status is returned before anything is launched when an argument is
  *    invalid; DBL_EHIP reports a failed launch. dbl_last_error() gives a message for the
  *    calling thread's last failure. Data-dependent problems (NaN inputs) are not detected.
