@@ -570,7 +570,7 @@ __device__ void finalize_block(const VerifyArgs& a, int64_t b, int nchunk) {
 #pragma unroll
         for (int j = 0; j < kStageBatch; ++j) {  // clamped indices: every load is in bounds
           const int idx = min(base + tid + 256 * j, R * kTile - 1);
-          const int64_t m = m0 + (idx >> 7);
+          const int64_t m = m0 + idx / kTile;
           const int i = min(idx & (kTile - 1), n - 1);
           lq[j] = flat_lq(k_.tls[m * V + v0 + i], k_.lmass[m * nT + pk.i], k_.lse[m]);
         }
