@@ -185,7 +185,9 @@ def test_objective_workload_chunked_expected_length():
 
 def test_stress_workload_1000_step_loop():
     """B=256, K=8, R=4: the head, draw and verification every step for 1000 steps with a Philox
-    stream per sequence; sampled (block, step) pairs checked against the oracle."""
+    stream per sequence; sampled (block, step) pairs checked against the oracle. The sampled
+    steps also request the acceptance masses, E and AL_b, i.e. take the benchmark's verification
+    stream (eight 32-tile chunks per workgroup at this shape); the others verify without them."""
     from paper_2608_05448_amd import dblast as D
     wl = synth.WORKLOADS["stress"]
     steps = 1000
@@ -204,13 +206,15 @@ def test_stress_workload_1000_step_loop():
         tls, lmass, lse = D.dbl_head_logprobs(h, w)
         D.dbl_sample_block(tls, lmass, lse, ell, z_temp=wl.z_temp, seed=wl.philox_seed, step=t,
                            z_out=z, x_out=x)
+        full = t in probe_steps
         out = D.dbl_verify_block(tls, lmass, lse, ell, x, logp, z_temp=wl.z_temp,
-                                 seed=wl.philox_seed, step=t, want_beta=False,
-                                 want_exp_len=False)
+                                 seed=wl.philox_seed, step=t, want_beta=full, want_al=full,
+                                 want_exp_len=full)
         tot_acc += out["n_accept"].double()
-        if t in probe_steps:
+        if full:
             rec[t] = (z.cpu().numpy(), x.cpu().numpy(), out["n_accept"].cpu().numpy(),
-                      out["next_token"].cpu().numpy())
+                      out["next_token"].cpu().numpy(), out["accept_mass"].cpu().numpy(),
+                      out["al_expected"].cpu().numpy(), out["exp_len"].cpu().numpy())
         if t % 250 == 0:
             torch.cuda.synchronize()
             print(f"[fullsize] stress step {t}", flush=True)
@@ -223,12 +227,15 @@ def test_stress_workload_1000_step_loop():
         for t in probe_steps:
             zo, xo = MX.sample_blocks(o_tls[None], o_lm[None], o_ls[None], ell_np[b:b + 1],
                                       wl.z_temp, wl.philox_seed, t, np.array([b]))
-            zg, xg, nag, ntg = (a[b] for a in rec[t])
+            zg, xg, nag, ntg, betag, alg, eg = (a[b] for a in rec[t])
             assert zg == zo[0]
             assert np.array_equal(xg, xo[0]), (b, t)
             ref = MX.verify_blocks(lq[None], ell_np[b:b + 1], wl.z_temp, xo, lp[b:b + 1],
-                                   wl.philox_seed, t, np.array([b]), with_beta=False)
+                                   wl.philox_seed, t, np.array([b]))
             assert nag == ref["n_accept"][0] and ntg == ref["next_token"][0], (b, t)
+            np.testing.assert_allclose(betag, ref["beta"][0], rtol=1e-4, atol=1e-30)
+            np.testing.assert_allclose(alg, ref["al"][0], rtol=1e-4, atol=1e-30)
+            np.testing.assert_allclose(eg, ref["E"][0], rtol=1e-4, atol=1e-30)
     # Different steps draw different blocks (the step counter advances every stream).
     assert not np.array_equal(rec[0][1], rec[1][1])
     print(f"[fullsize] stress mean accepted per block-step "
