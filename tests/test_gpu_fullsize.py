@@ -3,7 +3,7 @@
 Each test runs the whole hot path at the workload's real shape in the same launch
 configuration as the benchmark, then recomputes blocks end to end with the oracle (binary64
 head on the same bf16 inputs, then the oracle's own draw and verification): every block of the
-Qwen3-8B step at every target temperature, sampled blocks and steps of the objective and stress
+Qwen3-8B step at every target temperature and of the Qwen3-4B step, sampled blocks and steps of the objective and stress
 workloads. Token
 indices must agree exactly; any disagreement must be a certified near-tie (the GPU's fp32
 log-probs differ from the oracle's binary64 ones by ~1e-6, which can move a threshold across a
@@ -65,13 +65,16 @@ def _near_tie_token(tls_row, lm_row, ls, r_tile, r_id, got, want):
     return _near_tie(C.quant40(C.detexp32(ids)), r_id, got % MX.TILE, want % MX.TILE)
 
 
-def test_e2e_qwen3_8b_all_blocks_all_temperatures():
-    """The benchmark's step at the Qwen3-8B shape, every block: the oracle's binary64 head on the
-    same bf16 inputs, then its own draw and verification, at every target temperature."""
+@pytest.mark.parametrize("name,temps", [("qwen3_8b", synth.QWEN3_8B_TEMPERATURES),
+                                        ("qwen3_4b", (synth.WORKLOADS["qwen3_4b"].temperature,))])
+def test_e2e_all_blocks(name, temps):
+    """The benchmark's step at the Qwen3-8B shape (every target temperature) and the Qwen3-4B
+    shape (its own), every block: the oracle's binary64 head on the same bf16 inputs, then its own
+    draw and verification."""
     from cases import oracle_full_factored, oracle_full_head
     from paper_2608_05448_amd import dblast as D
-    wl = synth.WORKLOADS["qwen3_8b"]
-    print(f"[fullsize] qwen3_8b e2e B={wl.B} K={wl.K} R={wl.R} d={wl.d} V={wl.V}", flush=True)
+    wl = synth.WORKLOADS[name]
+    print(f"[fullsize] {name} e2e B={wl.B} K={wl.K} R={wl.R} d={wl.d} V={wl.V}", flush=True)
     h = synth.make_h(wl, "cuda")
     w = synth.make_w(wl, "cuda")
     ell = synth.make_ell(wl, "cuda")
@@ -79,9 +82,9 @@ def test_e2e_qwen3_8b_all_blocks_all_temperatures():
     z, x = D.dbl_sample_block(tls, lmass, lse, ell, z_temp=wl.z_temp, seed=wl.philox_seed, step=0)
     torch.cuda.synchronize()
     B, K, R, V = wl.B, wl.K, wl.R, wl.V
-    print(f"[fullsize] qwen3_8b: oracle head on all {wl.M} rows", flush=True)
-    lq_all = oracle_full_head("qwen3_8b", h, w).reshape(B, K, R, V)
-    o_tls, o_lm, o_ls = oracle_full_factored("qwen3_8b", h, w)
+    print(f"[fullsize] {name}: oracle head on all {wl.M} rows", flush=True)
+    lq_all = oracle_full_head(name, h, w).reshape(B, K, R, V)
+    o_tls, o_lm, o_ls = oracle_full_factored(name, h, w)
     o_tls, o_lm, o_ls = o_tls.reshape(B, K, R, V), o_lm.reshape(B, K, R, -1), o_ls.reshape(B, K, R)
     z_g, x_g = z.cpu().numpy(), x.cpu().numpy()
     ell_np = ell.cpu().numpy()
@@ -98,13 +101,13 @@ def test_e2e_qwen3_8b_all_blocks_all_temperatures():
                 assert _near_tie_token(o_tls[b, k, zb], o_lm[b, k, zb], o_ls[b, k, zb], r0, r1,
                                        x_g[b, k], x_o[b, k])
                 mismatches += 1
-    print(f"[fullsize] qwen3_8b draw: certified near-ties {mismatches}", flush=True)
+    print(f"[fullsize] {name} draw: certified near-ties {mismatches}", flush=True)
     # Verification is compared where both sides drafted the same block (all of them unless a
     # certified near-tie moved a token); each side verifies its own draft.
     same = [b for b in range(B) if np.array_equal(x_g[b], x_o[b])]
     assert len(same) >= B - mismatches
     sel = np.array(same)
-    for T in synth.QWEN3_8B_TEMPERATURES:
+    for T in temps:
         logp = synth.make_logp(wl, rows=wl.K + 1, device="cuda", temperature=T)
         out = D.dbl_verify_block(tls, lmass, lse, ell, x, logp, z_temp=wl.z_temp,
                                  seed=wl.philox_seed, step=0)
@@ -118,7 +121,7 @@ def test_e2e_qwen3_8b_all_blocks_all_temperatures():
         assert _rel(out["exp_len"].cpu().numpy()[sel], ref["E"]) < 1e-4
         assert _rel(out["al_expected"].cpu().numpy()[sel], ref["al"]) < 1e-4
         na = out["n_accept"].float().mean().item()
-        print(f"[fullsize] qwen3_8b T={T}: {len(same)} blocks match; mean n_accept {na:.3f}, "
+        print(f"[fullsize] {name} T={T}: {len(same)} blocks match; mean n_accept {na:.3f}, "
               f"mean E {out['exp_len'].mean().item():.4f}", flush=True)
 
 
