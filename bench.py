@@ -389,22 +389,31 @@ def _rows(wl, dev, steps: int, warmup: int, cpu: bool = True):
     del buf, dst
     # Reference for the head: the vendor library's plain bf16 GEMM of the same shape (hipBLASLt
     # through torch's linear: logits = h w^T, bf16 output, no log-softmax), against the library
-    # head (GEMM + fused per-tile log-softmax, fp32 output, LSE).
-    hh = synth.make_h(wl, dev).reshape(B * K * R, d)
-    ww = synth.make_w(wl, dev)
-    logits = torch.empty((B * K * R, V), dtype=torch.bfloat16, device=dev)
-    ms = timed(lambda: torch.matmul(hh, ww.t(), out=logits))
-    flop = 2.0 * B * K * R * d * V
-    rows["reference_gemm"] = {"ms": ms, "bound": "mfma", "tflops": flop / (ms * 1e-3) / 1e12,
-                              "frac": flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-                              "what": "torch.matmul (hipBLASLt), bf16 in and out, no epilogue"}
-    del logits
-    tls = torch.empty((B, K, R, V), dtype=torch.float32, device=dev)
-    lmass = torch.empty((B, K, R, D.ntiles(V)), dtype=torch.float32, device=dev)
-    lse = torch.empty((B, K, R), dtype=torch.float32, device=dev)
-    ms = timed(lambda: D.dbl_head_logprobs(hh.view(B, K, R, d), ww, tls, lmass, lse))
-    rows["head_logprobs"] = {"ms": ms, "bound": "mfma", "tflops": flop / (ms * 1e-3) / 1e12,
-                             "frac": flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+    # head (GEMM + fused per-tile log-softmax, fp32 output, LSE); at this workload's shape and,
+    # for comparison, at the Qwen3-4B head's.
+    def head_pair(hw, suffix):
+        hB, hK, hR, hd, hV = hw.B, hw.K, hw.R, hw.d, hw.V
+        hh = synth.make_h(hw, dev).reshape(hB * hK * hR, hd)
+        ww = synth.make_w(hw, dev)
+        logits = torch.empty((hB * hK * hR, hV), dtype=torch.bfloat16, device=dev)
+        ms = timed(lambda: torch.matmul(hh, ww.t(), out=logits))
+        flop = 2.0 * hB * hK * hR * hd * hV
+        rows["reference_gemm" + suffix] = {
+            "ms": ms, "bound": "mfma", "tflops": flop / (ms * 1e-3) / 1e12,
+            "frac": flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "what": "torch.matmul (hipBLASLt), bf16 in and out, no epilogue"}
+        del logits
+        tls = torch.empty((hB, hK, hR, hV), dtype=torch.float32, device=dev)
+        lmass = torch.empty((hB, hK, hR, D.ntiles(hV)), dtype=torch.float32, device=dev)
+        lse = torch.empty((hB, hK, hR), dtype=torch.float32, device=dev)
+        ms = timed(lambda: D.dbl_head_logprobs(hh.view(hB, hK, hR, hd), ww, tls, lmass, lse))
+        rows["head_logprobs" + suffix] = {"ms": ms, "bound": "mfma",
+                                          "tflops": flop / (ms * 1e-3) / 1e12,
+                                          "frac": flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+
+    head_pair(wl, "")
+    if wl.name != "qwen3_4b":
+        head_pair(synth.WORKLOADS["qwen3_4b"], "_qwen3_4b")
     return {"metric": "per-call time of the entry points outside the step", "rows": rows,
             "steps": steps, "warmup": warmup, "data": "synthetic",
             "config": {"workload": wl.name, "B": B, "K": K, "R": R, "d": d, "V": V,
