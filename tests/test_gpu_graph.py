@@ -1,8 +1,8 @@
 """The library under HIP graph capture: one step (head with argmax, block draw, verification)
 captured once and replayed, every replay bit-identical to the eager step.
 
-The entry points allocate nothing, synchronise nothing and clear their workspaces with kernels,
-so a caller may capture them; between replays the outputs are overwritten by eager work, so each
+The entry points allocate nothing, synchronise nothing and need no workspace clearing, so a
+caller may capture them; between replays the outputs are overwritten by eager work, so each
 replay must rewrite all of them.
 """
 import pytest
