@@ -43,6 +43,9 @@ CASES = [
     # 32-lane segments, R <= 16 over 8-lane segments.
     ("looped-gather-r24", 4, 12, 24, 800, 16, "aligned-block", 1, 1.0, 1.0, 16, 0, 2),
     ("looped-gather-r8", 16, 40, 8, 600, 16, "aligned-block", 1, 1.0, 1.0, 17, 4, 0),
+    # More than 2048 tiles per row: the workgroup inverse CDFs walk runs of 10 tile sums or masses
+    # instead of holding them in registers.
+    ("huge-vocab", 3, 3, 2, 300000, 8, "aligned", 1, 1.0, 1.0, 18, 0, 0),
 ]
 NOISE = {"bench-variant-r8": 0.1, "objective-variant-r16": 0.1, "r4-stress-variant": 0.1,
          "long-chain": 0.02, "chunked-finalize": 0.02, "looped-gather-r24": 0.05,
