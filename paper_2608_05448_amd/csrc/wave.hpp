@@ -166,52 +166,6 @@ __device__ __forceinline__ int draw_category(const BlockArgs& a, int64_t b) {
   return R - 1;  // unreachable: cum reaches Z > T
 }
 
-// Inverse-CDF selection over per-tile integer sums followed by an in-tile scan.
-// `tiles` holds the nT tile sums; weight(v) recomputes the integer weight of id v (v < V).
-// Returns the smallest id whose inclusive cumulative weight exceeds floor(r Z / 2^32), or -1
-// when the total weight Z is 0. Executed by one full wavefront; all lanes return the result.
-template <class WeightFn>
-__device__ __forceinline__ int select_by_tiles(const uint64_t* tiles, int nT, int64_t V,
-                                               uint32_t r, WeightFn weight) {
-  const int lane = lane_id();
-  uint64_t part = 0;
-  for (int t = lane; t < nT; t += 64) part += tiles[t];
-  const uint64_t Z = wave_sum_u64(part);
-  if (Z == 0) return -1;
-  const uint64_t T = icdf_threshold(r, Z);
-  // Find the tile holding T.
-  uint64_t running = 0;
-  int tsel = -1;
-  uint64_t before = 0;
-  for (int t0 = 0; t0 < nT; t0 += 64) {
-    const int t = t0 + lane;
-    const uint64_t val = t < nT ? tiles[t] : 0;
-    const uint64_t incl = wave_incl_scan_u64(val) + running;
-    const uint64_t hit = __ballot(t < nT && incl > T);
-    if (hit) {
-      const int l = __ffsll(static_cast<unsigned long long>(hit)) - 1;
-      tsel = t0 + l;
-      before = __shfl(incl - val, l);
-      break;
-    }
-    running = __shfl(incl, 63);
-  }
-  if (tsel < 0) return -1;  // unreachable for consistent tile sums
-  // In-tile scan: lane holds ids 128 tsel + 2 lane + {0, 1}.
-  const int64_t v0 = static_cast<int64_t>(tsel) * kTile + 2 * lane;
-  const uint64_t q0 = v0 < V ? weight(v0) : 0;
-  const uint64_t q1 = v0 + 1 < V ? weight(v0 + 1) : 0;
-  const uint64_t incl = wave_incl_scan_u64(q0 + q1);
-  const uint64_t c0 = before + incl - q1;  // cumulative through id v0
-  const uint64_t c1 = before + incl;       // cumulative through id v0 + 1
-  const bool h0 = c0 > T, h1 = c1 > T;
-  const uint64_t hit = __ballot(h0 || h1);
-  if (!hit) return -1;  // unreachable for consistent tile sums
-  const int l = __ffsll(static_cast<unsigned long long>(hit)) - 1;
-  const int pick0 = __shfl(static_cast<int>(h0), l);
-  return static_cast<int>(static_cast<int64_t>(tsel) * kTile + 2 * l + (pick0 ? 0 : 1));
-}
-
 // Workgroup inverse CDF over n integer weights weigh(load(i)), i < n (every thread of a
 // 256-thread workgroup calls it, with the same n and r): each thread sums a contiguous run, a
 // workgroup scan gives the total Z and the run holding T = floor(r Z / 2^32), and that run's
