@@ -200,3 +200,40 @@ def test_out_of_range_draft_ids_are_rejected_without_faulting():
     na = o["n_accept"].cpu().numpy()
     assert na[0] == 0 and na[1] == 0 and na[2] <= 2
     assert np.all(o["al_expected"].cpu().numpy()[:2] == 0.0)
+
+
+def test_random_shapes_against_the_oracle():
+    """A seeded sweep of small random shapes (B, K, R, V, Kp, target, temperatures), so that
+    combinations the cases above do not name (K = 1, V below one tile, odd R, ragged last tiles,
+    with and without the bonus row) go through the draw and verification against the oracle."""
+    from paper_2608_05448_amd import dblast as D
+    rng = np.random.default_rng(20261202)
+    for i in range(14):
+        B = int(rng.integers(1, 24))
+        K = int(rng.integers(1, 20))
+        R = int(rng.integers(1, 20))
+        V = int(rng.choice([int(rng.integers(1, 128)), int(rng.integers(128, 6000))]))
+        kx = int(rng.integers(0, 2))
+        target = str(rng.choice(["aligned", "aligned-block", "independent"]))
+        zt = float(rng.choice([0.0, 0.5, 1.0, 2.0]))
+        T = float(rng.choice([0.0, 0.7, 1.0]))
+        seed, step, so = int(rng.integers(0, 2**40)), int(rng.integers(0, 1000)), int(rng.integers(0, 999))
+        print(f"[random] {i}: B={B} K={K} R={R} V={V} Kp=K+{kx} {target} z_temp={zt} T={T} "
+              f"seed={seed} step={step} so={so}", flush=True)
+        c = BlockCase(B, K, R, V, d=8, seed=100 + i, target=target, kp_extra=kx, T=T, noise=0.05)
+        tls, lmass, lse, ell, logp = c.device()
+        seq = so + np.arange(B)
+        z, x = D.dbl_sample_block(tls, lmass, lse, ell, z_temp=zt, seed=seed, step=step,
+                                  seq_offset=so)
+        out = D.dbl_verify_block(tls, lmass, lse, ell, x, logp, z_temp=zt, seed=seed, step=step,
+                                 seq_offset=so)
+        torch.cuda.synchronize()
+        z_o, x_o = MX.sample_blocks(c.tls, c.lmass, c.lse, c.ell, zt, seed, step, seq)
+        np.testing.assert_array_equal(z.cpu().numpy(), z_o)
+        np.testing.assert_array_equal(x.cpu().numpy(), x_o)
+        ref = MX.verify_blocks(c.lq, c.ell, zt, x_o, c.logp, seed, step, seq)
+        np.testing.assert_array_equal(out["n_accept"].cpu().numpy(), ref["n_accept"])
+        np.testing.assert_array_equal(out["next_token"].cpu().numpy(), ref["next_token"])
+        _rel_close(out["accept_mass"].cpu().numpy(), ref["beta"])
+        _rel_close(out["al_expected"].cpu().numpy(), ref["al"])
+        _rel_close(out["exp_len"].cpu().numpy(), ref["E"])
