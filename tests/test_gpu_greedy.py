@@ -192,3 +192,37 @@ def test_greedy_end_to_end_from_the_head_argmax():
     np.testing.assert_array_equal(x.cpu().numpy(), x_o)
     np.testing.assert_array_equal(out["n_accept"].cpu().numpy(), ref["n_accept"])
     np.testing.assert_array_equal(out["next_token"].cpu().numpy(), ref["next_token"])
+
+
+def test_greedy_random_shapes_against_the_oracle():
+    """A seeded sweep of small random greedy-branch shapes (staged and unstaged chains, V below
+    one tile, shared or independent branch prefixes, with and without the bonus row) against
+    the oracle."""
+    from paper_2608_05448_amd import dblast as D
+    rng = np.random.default_rng(20261203)
+    for i in range(14):
+        B = int(rng.integers(1, 24))
+        K = int(rng.integers(1, 40))
+        R = int(rng.integers(1, 40))
+        V = int(rng.choice([int(rng.integers(2, 128)), int(rng.integers(128, 5000))]))
+        kx = int(rng.integers(0, 2))
+        share, aligned = bool(rng.integers(0, 2)), bool(rng.integers(0, 2))
+        zt = float(rng.choice([0.0, 0.5, 1.0, 2.0]))
+        seed, step, so = int(rng.integers(0, 2**40)), int(rng.integers(0, 1000)), int(rng.integers(0, 999))
+        print(f"[greedy random] {i}: B={B} K={K} R={R} V={V} Kp=K+{kx} share={share} "
+              f"aligned={aligned} z_temp={zt} seed={seed} step={step} so={so}", flush=True)
+        xhat, ell, logp = _greedy_inputs(B, K, R, V, 200 + i, share, aligned, kx)
+        xd, ed, ld = (torch.from_numpy(a).cuda() for a in (xhat, ell, logp))
+        seq = so + np.arange(B)
+        z_g, x_g = D.dbl_sample_greedy(xd, ed, z_temp=zt, seed=seed, step=step, seq_offset=so, V=V)
+        out = D.dbl_verify_greedy(xd, ed, x_g, ld, z_temp=zt, seed=seed, step=step, seq_offset=so)
+        torch.cuda.synchronize()
+        z_o, x_o = GR.sample_blocks_greedy(xhat, ell, zt, seed, step, seq)
+        np.testing.assert_array_equal(z_g.cpu().numpy(), z_o)
+        np.testing.assert_array_equal(x_g.cpu().numpy(), x_o)
+        ref = GR.verify_blocks_greedy(xhat, ell, zt, x_o, logp, seed, step, seq)
+        np.testing.assert_array_equal(out["n_accept"].cpu().numpy(), ref["n_accept"])
+        np.testing.assert_array_equal(out["next_token"].cpu().numpy(), ref["next_token"])
+        _rel_close(out["accept_mass"].cpu().numpy(), ref["beta"])
+        _rel_close(out["al_expected"].cpu().numpy(), ref["al"])
+        _rel_close(out["exp_len"].cpu().numpy(), ref["E"])
