@@ -115,3 +115,23 @@ def _full_size(name):
         err = max(err, float(np.max(np.abs(got.astype(np.float64) - ref[r0:r0 + 256]))))
     print(f"[head] full-size {name} all rows max |log q error| = {err:.3e}", flush=True)
     assert err < 2e-3
+
+
+def test_head_random_shapes():
+    """A seeded sweep of random head shapes in both input precisions: hidden sizes that take each
+    bf16 kernel (d % 64 = 0, d % 32 = 0 only, d % 8 = 0 only) and arbitrary fp32 ones, branch-row
+    and vocabulary counts with ragged last tiles."""
+    rng = np.random.default_rng(20261204)
+    for i in range(12):
+        bf16 = i % 3 != 2
+        B, K, R = int(rng.integers(1, 25)), int(rng.integers(1, 9)), int(rng.integers(1, 9))
+        if bf16:
+            d = int(rng.choice([64 * int(rng.integers(1, 9)), 32 * int(rng.integers(1, 17)),
+                                8 * int(rng.integers(1, 65))]))
+        else:
+            d = int(rng.integers(1, 300))
+        V = int(rng.choice([int(rng.integers(1, 130)), int(rng.integers(130, 6000))]))
+        dt = torch.bfloat16 if bf16 else torch.float32
+        h = synth.make_uniform_logits((B, K, R, d), 300 + i).to(dt)
+        w = (synth.make_uniform_logits((V, d), 400 + i) * (0.05 if bf16 else 1.0 / math.sqrt(d)))
+        _check(h, w.to(dt), 2e-3 if bf16 else 2e-5, f"random-{i}")

@@ -205,7 +205,8 @@ def test_out_of_range_draft_ids_are_rejected_without_faulting():
 def test_random_shapes_against_the_oracle():
     """A seeded sweep of small random shapes (B, K, R, V, Kp, target, temperatures), so that
     combinations the cases above do not name (K = 1, V below one tile, odd R, ragged last tiles,
-    with and without the bonus row) go through the draw and verification against the oracle."""
+    with and without the bonus row) go through the draw, the verification and the
+    expected-length reduction against the oracle."""
     from paper_2608_05448_amd import dblast as D
     rng = np.random.default_rng(20261202)
     for i in range(14):
@@ -237,3 +238,11 @@ def test_random_shapes_against_the_oracle():
         _rel_close(out["accept_mass"].cpu().numpy(), ref["beta"])
         _rel_close(out["al_expected"].cpu().numpy(), ref["al"])
         _rel_close(out["exp_len"].cpu().numpy(), ref["E"])
+        # The expected-length reduction along a random trajectory of the same shape.
+        xs = rng.integers(0, V, size=(B, K)).astype(np.int32)
+        beta_g, e_g = D.dbl_expected_len(tls, lmass, lse, ell, torch.from_numpy(xs).cuda(),
+                                         logp[:, :K].contiguous(), z_temp=zt)
+        torch.cuda.synchronize()
+        beta_o, e_o = MX.expected_len_blocks(c.lq, c.ell, zt, xs, c.logp[:, :K])
+        _rel_close(beta_g.cpu().numpy(), beta_o)
+        _rel_close(e_g.cpu().numpy(), e_o)
