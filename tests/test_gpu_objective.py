@@ -40,14 +40,12 @@ def _close(got, want, tol=1e-5):
     assert err.size == 0 or err.max() < tol, err.max()
 
 
-@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_objective_parity(case):
+def _objective_case(name, B, K, R, V, d, target, T, zt, tau, seed):
+    """One objective call at this shape against the oracle (trajectories drawn from the target)."""
     from paper_2608_05448_amd import dblast as D
-    name, B, K, R, V, d, target, T, zt, tau = case
-    print(f"[objective] {name} B={B} K={K} R={R} V={V} tau={tau}", flush=True)
-    c = BlockCase(B, K, R, V, d=d, seed=zlib.crc32(name.encode()) % 1000, target=target,
-                  kp_extra=0, T=T)
-    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    print(f"[objective] {name} B={B} K={K} R={R} V={V} T={T} z_temp={zt} tau={tau}", flush=True)
+    c = BlockCase(B, K, R, V, d=d, seed=seed % 1000, target=target, kp_extra=0, T=T)
+    rng = np.random.default_rng(seed)
     p = np.exp(c.logp.astype(np.float64))
     cum = np.cumsum(p / p.sum(-1, keepdims=True), axis=-1)
     xs = np.minimum((cum < rng.random((B, K, 1))).sum(-1), V - 1).astype(np.int32)
@@ -70,3 +68,22 @@ def test_objective_parity(case):
     if R == 1:   # Eq. independent-nll: the sum of per-position cross-entropies
         ce = -np.sum(c.lq[np.arange(B)[:, None], np.arange(K)[None, :], 0, xs], axis=1)
         _close(out["nll"].cpu().numpy(), ce)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_objective_parity(case):
+    _objective_case(*case, zlib.crc32(case[0].encode()))
+
+
+def test_objective_random_shapes():
+    """A seeded sweep of random small shapes (K = 1 included, V below one tile, odd R, target
+    temperature 0, a range of tau) against the oracle."""
+    rng = np.random.default_rng(20261205)
+    for i in range(12):
+        B, K, R = int(rng.integers(1, 20)), int(rng.integers(1, 24)), int(rng.integers(1, 20))
+        V = int(rng.choice([int(rng.integers(2, 128)), int(rng.integers(128, 4000))]))
+        target = str(rng.choice(["aligned", "independent"]))
+        T = float(rng.choice([0.0, 0.7, 1.0, 1.5]))
+        zt = float(rng.choice([0.0, 0.5, 1.0, 2.0]))
+        tau = float(rng.choice([1e-4, 0.05, 0.1, 0.5, 0.9]))
+        _objective_case(f"random-{i}", B, K, R, V, 8, target, T, zt, tau, 500 + i)
