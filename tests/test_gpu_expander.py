@@ -33,10 +33,9 @@ EXPAND_CASES = [
 ]
 
 
-@pytest.mark.parametrize("case", EXPAND_CASES, ids=[c[0] for c in EXPAND_CASES])
-def test_expander_parity(case):
+def _expander_case(name, B, K, R, d):
+    """One expander call at this shape against the oracle (all rows, or 48 sampled ones)."""
     from paper_2608_05448_amd import dblast as D
-    name, B, K, R, d = case
     print(f"[expander] {name} B={B} K={K} R={R} d={d}", flush=True)
     h = synth.make_uniform_logits((B, K, d), 11).to(torch.bfloat16)
     W = (synth.make_uniform_logits((R * d, d), 12) * (0.5 / d ** 0.5)).to(torch.bfloat16)
@@ -66,6 +65,21 @@ def test_expander_parity(case):
     assert np.all(np.abs(g - exact) <= err_bound)
     same = np.mean(g == EX.bf16_round(exact))
     assert same > 0.99, same
+
+
+@pytest.mark.parametrize("case", EXPAND_CASES, ids=[c[0] for c in EXPAND_CASES])
+def test_expander_parity(case):
+    _expander_case(*case)
+
+
+def test_expander_random_shapes():
+    """A seeded sweep of random expander shapes: hidden sizes that are multiples of 32 (both the
+    64-deep and the 32-deep kernels), odd category counts and ragged trunk-row tiles."""
+    rng = np.random.default_rng(20261206)
+    for i in range(10):
+        B, K = int(rng.integers(1, 6)), int(rng.integers(1, 70))
+        R, d = int(rng.integers(1, 20)), 32 * int(rng.integers(1, 21))
+        _expander_case(f"random-{i}", B, K, R, d)
 
 
 def test_zero_expander_copies_the_trunk_state():
