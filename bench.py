@@ -489,6 +489,20 @@ def _objective_chunks(wl, dev, steps: int, warmup: int, chunk: int = 128, cpu: b
     M = nb * K * R
     head_tflops = 2.0 * M * d * V / (head_ms * 1e-3) / 1e12
     el_bytes = nb * K * (R + 1) * V * 4.0
+    # Reference after the timed steps: the vendor library's plain bf16 GEMM at the chunk's head
+    # shape (torch.matmul, hipBLASLt, bf16 output, no log-softmax), one chunk's h against w.
+    h0 = chunks[0][0].reshape(M, d)
+    logits = torch.empty((M, V), dtype=torch.bfloat16, device=dev)
+    torch.matmul(h0, w.t(), out=logits)
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    r0.record(stream)
+    for _ in range(3):
+        torch.matmul(h0, w.t(), out=logits)
+    r1.record(stream)
+    torch.cuda.synchronize(dev)
+    ref_ms = r0.elapsed_time(r1) / 3
+    del logits
+    ref_tflops = 2.0 * M * d * V / (ref_ms * 1e-3) / 1e12
     return {"metric": "positions/s of head + expected length + objective forward",
             "value": B * K / (step_ms * 1e-3), "unit": "positions/s", "n_gpus": 1,
             "steps": steps, "warmup": warmup, "ms_per_step": step_ms, "higher_is_better": True,
@@ -499,6 +513,10 @@ def _objective_chunks(wl, dev, steps: int, warmup: int, chunk: int = 128, cpu: b
             "roofline": {"bound": "mfma", "achieved": head_tflops, "peak": PEAK_BF16_TFLOPS,
                          "unit": "TFLOP/s", "frac": head_tflops / PEAK_BF16_TFLOPS,
                          "kernel": "dbl_head_logprobs"},
+            "reference_gemm_chunk": {"ms": ref_ms, "tflops": ref_tflops,
+                                     "frac": ref_tflops / PEAK_BF16_TFLOPS,
+                                     "what": "torch.matmul (hipBLASLt), bf16 in and out, no "
+                                             "epilogue, one chunk's head shape"},
             "hbm": {"expected_len_GBps": el_bytes / (el_ms * 1e-3) / 1e9,
                     "expected_len_frac": el_bytes / (el_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
             "quality": {"mean_exp_len_last_chunk": float(e.mean().item()),
