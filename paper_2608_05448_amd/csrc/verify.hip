@@ -609,8 +609,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(VerifyArgs a, int nchunk)
 }
 
 // The acceptance-mass stream with the residual tile sums folded in (V % 4 == 0, masses
-// requested). Workgroup g handles chunk c = g % nchunk (32 vocabulary tiles; cpw consecutive
-// chunks at R <= 4) of position row k of block b, g / nchunk = k B + b:
+// requested). Workgroup g handles chunk c = g % nchunk (stream_tiles(R) vocabulary tiles: 40, or
+// 32 at R <= 4, where cpw consecutive chunks share a workgroup) of position row k of block b,
+// g / nchunk = k B + b:
 //  * k < K: the R branch rows and the target row of the chunk are read once for the
 //    acceptance-mass partial; at the block's first rejected position the same loaded values also
 //    give the contract's integer residual and target tile sums (weights as in residual_body), so
@@ -639,9 +640,16 @@ constexpr int kStreamChunksSmallR = 8;
 constexpr int64_t kStreamMinGroups = 2048;  // one workgroup per slot at eight waves per SIMD
 __host__ __device__ constexpr bool stream_multi_chunk(int rt) { return rt > 0 && rt <= 4; }
 
+// Vocabulary tiles per stream chunk: 32 where several chunks share a workgroup, else 40 (30
+// chunks per row at V = 151,936: fewer, longer workgroups whose count fills whole rounds of the
+// 2048 slots at the Qwen3 shapes: verification call 0.2257 -> 0.2226 ms at Qwen3-8B and
+// 0.1221 -> 0.1201 ms at Qwen3-4B; 48 tiles measured 0.2235 and 0.1233).
+__host__ __device__ constexpr int stream_tiles(int rt) { return stream_multi_chunk(rt) ? 32 : 40; }
+
 template <int RT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(stream_waves<RT>(), 8)))
 void verify_stream_kernel(VerifyArgs a, int nchunk, int cpw) {
+  constexpr int TPC = stream_tiles(RT);  // vocabulary tiles per chunk
   const int CPW = stream_multi_chunk(RT) ? cpw : 1;
   const BlockArgs& k_ = a.blk;
   const int64_t B = k_.B;
@@ -654,7 +662,7 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int cpw) {
   const int tid = threadIdx.x;
   __shared__ float s_w[kMaxR];
   __shared__ double s_wz[kMaxR];
-  __shared__ float s_offx[kMaxR][kTilesPerChunk];  // fl32(lmass - lse) of the chunk's tiles
+  __shared__ float s_offx[kMaxR][TPC];  // fl32(lmass - lse) of the chunk's tiles
   __shared__ float red[4];
   const int ks = a.trajectory ? -1 : a.n_accept[b];  // first rejected position, K if none
   const bool bonus = k == k_.K;
@@ -665,11 +673,11 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int cpw) {
   const int c = cw * CPW + cc;
   if (c >= nchunk) break;       // workgroup-uniform
   if (cc > 0) __syncthreads();  // the previous chunk's readers of s_offx and red are done
-  const int t0 = c * kTilesPerChunk;
-  const int nt = min(kTilesPerChunk, k_.nT - t0);
+  const int t0 = c * TPC;
+  const int nt = min(TPC, k_.nT - t0);
   if (!bonus) {
-    for (int i = tid; i < R * kTilesPerChunk; i += blockDim.x) {
-      const int z = i / kTilesPerChunk, tt = i % kTilesPerChunk;
+    for (int i = tid; i < R * TPC; i += blockDim.x) {
+      const int z = i / TPC, tt = i % TPC;
       if (tt < nt) s_offx[z][tt] = k_.lmass[(m0 + z) * k_.nT + t0 + tt] - k_.lse[m0 + z];
     }
     if (cc == 0 && tid < R) {
@@ -686,7 +694,7 @@ void verify_stream_kernel(VerifyArgs a, int nchunk, int cpw) {
   float acc = 0.0f;
   if (!bonus || res) {
 #pragma unroll 1
-    for (int i = 0; i < kTilesPerChunk * kTile / 1024; ++i) {
+    for (int i = 0; i < TPC * kTile / 1024; ++i) {
       const int64_t v = vb + 4 * tid + 1024 * i;
       const int tt = (4 * tid + 1024 * i) >> 7;  // the 32 threads of a half-wave share a tile
       uint64_t sp = 0, sr = 0;
@@ -795,7 +803,9 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const bool want_beta = a.beta || a.exp_len;
-  if (want_beta && (a.blk.V & 3) == 0 && !a.trajectory) {
+  const bool stream_path = want_beta && (a.blk.V & 3) == 0 && !a.trajectory;
+  int nchunk_f = nchunk;  // the finalisation's partials per position
+  if (stream_path) {
     // One stream: acceptance masses, and the residual tile sums at the first rejection from the
     // same loads. Trajectory mode keeps the beta kernel below: its stream has no residual
     // arithmetic to carry, and at R = 16 it measured 3.48 ms against 3.78 ms fused per 128-block
@@ -803,19 +813,21 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
     const int rows = static_cast<int>(a.blk.K) + (!a.trajectory && a.Kp == a.blk.K + 1 ? 1 : 0);
     const int64_t R = a.blk.R;  // the template argument of the launch below: R, or 0
     const int rt = R == 1 || R == 2 || R == 4 || R == 8 || R == 16 ? static_cast<int>(R) : 0;
-    const int64_t cw_many = (nchunk + kStreamChunksSmallR - 1) / kStreamChunksSmallR;
+    const int nchunk_s = (a.blk.nT + stream_tiles(rt) - 1) / stream_tiles(rt);
+    nchunk_f = nchunk_s;
+    const int64_t cw_many = (nchunk_s + kStreamChunksSmallR - 1) / kStreamChunksSmallR;
     const int cpw = stream_multi_chunk(rt) && rows * B * cw_many >= kStreamMinGroups
                         ? kStreamChunksSmallR : 1;
-    const int64_t nwg = static_cast<int64_t>(rows) * B * ((nchunk + cpw - 1) / cpw);
+    const int64_t nwg = static_cast<int64_t>(rows) * B * ((nchunk_s + cpw - 1) / cpw);
     if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nwg));
     switch (a.blk.R) {
-      case 1: hipLaunchKernelGGL(verify_stream_kernel<1>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
-      case 2: hipLaunchKernelGGL(verify_stream_kernel<2>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
-      case 4: hipLaunchKernelGGL(verify_stream_kernel<4>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
-      case 8: hipLaunchKernelGGL(verify_stream_kernel<8>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
-      case 16: hipLaunchKernelGGL(verify_stream_kernel<16>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
-      default: hipLaunchKernelGGL(verify_stream_kernel<0>, grid, dim3(256), 0, stream, a, nchunk, cpw); break;
+      case 1: hipLaunchKernelGGL(verify_stream_kernel<1>, grid, dim3(256), 0, stream, a, nchunk_s, cpw); break;
+      case 2: hipLaunchKernelGGL(verify_stream_kernel<2>, grid, dim3(256), 0, stream, a, nchunk_s, cpw); break;
+      case 4: hipLaunchKernelGGL(verify_stream_kernel<4>, grid, dim3(256), 0, stream, a, nchunk_s, cpw); break;
+      case 8: hipLaunchKernelGGL(verify_stream_kernel<8>, grid, dim3(256), 0, stream, a, nchunk_s, cpw); break;
+      case 16: hipLaunchKernelGGL(verify_stream_kernel<16>, grid, dim3(256), 0, stream, a, nchunk_s, cpw); break;
+      default: hipLaunchKernelGGL(verify_stream_kernel<0>, grid, dim3(256), 0, stream, a, nchunk_s, cpw); break;
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   } else if (want_beta && !a.trajectory) {
@@ -855,7 +867,7 @@ hipError_t launch_verify(const VerifyArgs& a, hipStream_t stream) {
   }
   if (want_beta || !a.trajectory) {
     hipLaunchKernelGGL(finalize_kernel, dim3(static_cast<unsigned>(B)), dim3(256), 0, stream, a,
-                       nchunk);
+                       nchunk_f);
     e = hipGetLastError();
   }
   return e;
