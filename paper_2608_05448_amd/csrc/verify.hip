@@ -645,6 +645,10 @@ __host__ __device__ constexpr bool stream_multi_chunk(int rt) { return rt > 0 &&
 // 2048 slots at the Qwen3 shapes: verification call 0.2257 -> 0.2226 ms at Qwen3-8B and
 // 0.1221 -> 0.1201 ms at Qwen3-4B; 48 tiles measured 0.2235 and 0.1233).
 __host__ __device__ constexpr int stream_tiles(int rt) { return stream_multi_chunk(rt) ? 32 : 40; }
+// The workspace holds n_chunks(nT) partials per position (kTilesPerChunk-tile chunks): no stream
+// chunk may be narrower, or the stream would write past them.
+static_assert(stream_tiles(0) >= kTilesPerChunk && stream_tiles(1) >= kTilesPerChunk,
+              "stream chunks narrower than the workspace's");
 
 template <int RT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(stream_waves<RT>(), 8)))
