@@ -210,7 +210,7 @@ dbl_status dbl_verify_block(dbl_shape shape, const float* tls, const float* lmas
  * fixed device array inside the library of 8 MiB (8388608 bytes), one copy per GPU, kept until
  * the process ends; the call allocates and frees nothing. Limit: shapes whose verification
  * workspace, dbl_workspace_bytes(DBL_OP_VERIFY, shape), exceeds 8 MiB are rejected (the
- * Qwen3-8B step needs 0.36 MiB, B = 256 blocks of K = 8 at V = 151,936 need 5.2 MiB).
+ * Qwen3-8B step needs 0.34 MiB, B = 256 blocks of K = 8 at V = 151,936 need 5.0 MiB).
  * Every call on one GPU shares that GPU's array: calls that overlap in time on one GPU (other
  * streams, other threads) race and must not be issued; calls ordered on one stream are safe.
  * `stream` must belong to the current device. Errors: as dbl_verify_block, plus DBL_EWORKSPACE
